@@ -1,0 +1,161 @@
+"""Benchmark of the ensemble-inference hot path on one MI355X.
+
+One step = one device pass of the whole path over one batch already resident
+in HBM: the shared resize+normalise of the batch, every model's forward pass,
+the softmax per model and the ensemble combine (fs_infer_device).  The
+default workload is three ResNet-18-shaped models in bf16 on a batch of 32
+uint8 256x256 images resized to 224x224.
+
+Prints ONE JSON line (rank 0, N=1):
+  value = images/s of the whole ensemble = B * K / (time of K steps),
+  roofline = the conv kernels (the dominant cost) measured with HIP events on
+             the launch stream over the timed steps, against bf16 MFMA peak,
+  cpu_baseline = the CPU oracle on this host, timed on a bounded sample.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="resnet18x3_bf16_b32")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="bound on the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="time without the per-launch events (no roofline)")
+    return ap.parse_args()
+
+
+def omp_threads():
+    try:
+        return int(ctypes.CDLL("libgomp.so.1").omp_get_max_threads())
+    except OSError:
+        return os.cpu_count()
+
+
+def cpu_baseline(w, imgs, seconds):
+    import oracle
+    import workloads as wl
+    prepared = [oracle.prepare_model(m, w["precision"]) for m in w["models"]]
+    n, t0 = 0, time.perf_counter()
+    while n < len(imgs):
+        oracle.ensemble(w["models"], imgs[n:n + 1], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD,
+                        w["precision"], prepared)
+        n += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "images/s", "cores": omp_threads(), "kind": "oracle",
+            "sample": f"{n} of the {len(imgs)} images through all {len(w['models'])} models "
+                      f"({w['precision']} storage, double accumulation), {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported "
+              "(every box has one GPU; the multi-GPU design is documented, not built)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads as wl
+    from paper_2003_01538_amd import flexserve as fsb
+
+    torch.cuda.set_device(0)
+    w = wl.workload(args.workload)
+    B = w["batch"]
+    imgs = list(wl.images_uniform(w["image_seed"], B, *w["in_hw"]))
+    ens = fsb.Ensemble(w["models"], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"],
+                       max_batch=B)
+    info = ens.info()
+    N, C = info["num_models"], info["num_classes"]
+
+    flat, desc = wl.pack_images(imgs)
+    d_pix = torch.from_numpy(flat).cuda()
+    d_desc = torch.tensor([[o, h | (wd << 32), rs] for o, h, wd, rs in desc], dtype=torch.int64).cuda()
+    d_probs = torch.empty((N, B, C), dtype=torch.float32, device="cuda")
+    d_logits = torch.empty_like(d_probs)
+    d_mean = torch.empty((B, C), dtype=torch.float32, device="cuda")
+    d_vote = torch.empty(B, dtype=torch.int32, device="cuda")
+    d_top1 = torch.empty((N, B), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        fsb.fs_infer_device(ens.handle, d_pix.data_ptr(), d_desc.data_ptr(), B, d_probs.data_ptr(),
+                            d_mean.data_ptr(), d_vote.data_ptr(), d_top1.data_ptr(),
+                            d_logits.data_ptr(), stream.cuda_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # plain timing (no events) and event-profiled timing of the same steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    plain_s = time.perf_counter() - t0
+
+    roof, stats = None, {}
+    if not args.no_profile:
+        fsb.fs_profile_enable(ens.handle, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        prof_s = time.perf_counter() - t0
+        stats = fsb.fs_profile_read(ens.handle)
+        fsb.fs_profile_enable(ens.handle, False)
+        cv = stats["conv"]
+        per_launch_ms = cv["total_ms"] / cv["launches"]
+        flops_per_launch = cv["flops"] / cv["launches"]
+        achieved = flops_per_launch / (per_launch_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": "conv (implicit GEMM, all conv launches of a step)",
+                "avg_launch_us": round(per_launch_ms * 1e3, 2)}
+        print(json.dumps({"profiled_ms_per_step": prof_s / args.steps * 1e3,
+                          "kernels": {k: dict(v, avg_us=v["total_ms"] / v["launches"] * 1e3,
+                                              share=v["total_ms"] / args.steps / (plain_s / args.steps * 1e3))
+                                      for k, v in stats.items()}}), file=sys.stderr)
+
+    ms = plain_s / args.steps * 1e3
+    out = {
+        "metric": "ensemble images/sec at B=32 (3xResNet-18, bf16) + MFMA util vs peak",
+        "value": round(B * args.steps / plain_s, 1),
+        "unit": "images/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w["precision"] == "bf16" else "f32",
+        "data": "synthetic: seeded uint8 noise images, He-normal random weights",
+        "config": {"workload": w["name"], "models": list(w["archs"]), "batch": B,
+                   "input_hw": list(w["in_hw"]), "transformed_hw": list(w["out_hw"]),
+                   "flops_per_image": info["flops_per_image"],
+                   "launches_per_step": info["launches_per_pass"]},
+        "roofline": roof,
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(w, imgs, args.cpu_seconds)
+    ens.close()
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,209 @@
+/*
+ * flexserve.h -- C ABI of the MI355X ensemble-inference library.
+ *
+ * The operation (FlexServe, Fig. 1 caption and Sec. 2.2): N image
+ * classification models are loaded into one device memory; a request's batch
+ * of images is transformed ONCE (bilinear resize + mean/std normalisation)
+ * and that one tensor feeds every model; the batch size varies per request
+ * (Sec. 2.3); the outputs of all models are returned together, per model
+ * and per image, together with a combined result (Fig. 1 caption; Sec. 2.1
+ * on combining ensemble outputs).
+ *
+ * Conventions for every entry point:
+ *  - The caller owns every host buffer.  fs_ensemble_create deep-copies and
+ *    converts the weights; the caller may free them when it returns.  The
+ *    library owns all device memory of an ensemble until fs_destroy.
+ *  - No exception, abort or print crosses the ABI.  Each failure returns a
+ *    status and sets a message readable with fs_last_error.
+ *  - Arguments are validated on the host before any device work; an invalid
+ *    call leaves the handle usable.
+ *  - Calls on one handle are serialised by an internal lock; distinct
+ *    handles are independent.
+ *  - Layouts are row-major.  Activations are NHWC.  Outputs are model-major:
+ *    probs[i][b][c] is model i, image b, class c.
+ */
+#ifndef FLEXSERVE_H
+#define FLEXSERVE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct fs_ensemble fs_ensemble; /* opaque */
+
+typedef enum {
+    FS_OK = 0,
+    FS_ERR_INVALID = 1,     /* bad argument, descriptor or shape          */
+    FS_ERR_OOM = 2,         /* device or pinned host allocation failed    */
+    FS_ERR_DEVICE = 3,      /* no such device, or a HIP runtime failure   */
+    FS_ERR_UNSUPPORTED = 4, /* well-formed but outside what is supported  */
+    FS_ERR_INTERNAL = 5
+} fs_status;
+
+typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_precision; /* storage type of the whole ensemble */
+typedef enum { FS_OP_CONV = 0, FS_OP_MAXPOOL = 1, FS_OP_GAP = 2, FS_OP_FC = 3 } fs_op;
+typedef enum { FS_COMBINE_MEAN = 0 } fs_combine;     /* mean of the models' probabilities */
+
+/* One layer, listed in topological order.  Layer outputs are referred to by
+ * index; src = -1 is the shared transformed input batch (3 channels). */
+typedef struct {
+    int32_t op;            /* fs_op */
+    int32_t src;           /* producer of the input, -1 = transformed batch */
+    int32_t residual_src;  /* conv: layer added before the ReLU, or -1      */
+    int32_t cin, cout;     /* conv/fc channels (fc: in/out features)        */
+    int32_t kh, kw;        /* conv kernel, maxpool window                   */
+    int32_t stride, pad;   /* conv / maxpool                                */
+    int32_t relu;          /* conv/fc: apply max(0, .) after bias+residual  */
+    int32_t flatten_nchw;  /* fc: the input map is flattened channel-major  */
+    const float *weight;   /* conv [cout][kh][kw][cin]; fc [cout][cin]      */
+    const float *bias;     /* [cout] or NULL (= 0)                          */
+    const float *bn_scale; /* conv: [cout] or NULL; w' = w*scale            */
+    const float *bn_shift; /* conv: [cout] or NULL; bias' = shift           */
+} fs_layer;
+
+typedef struct {
+    int32_t num_layers;
+    const fs_layer *layers;
+    int32_t num_classes; /* cout of the last layer, equal for all models */
+} fs_model_spec;
+
+/* The single data transformation shared by every model (Fig. 1 caption):
+ * bilinear resize (half-pixel centres, no antialias) to out_h x out_w, then
+ * (v/255 - mean[c]) / std[c] per RGB channel. */
+typedef struct {
+    int32_t out_h, out_w;
+    float mean[3];
+    float std[3];
+} fs_preprocess;
+
+typedef struct {
+    int32_t num_models;
+    const fs_model_spec *models;
+    fs_preprocess pre;
+    int32_t precision;  /* fs_precision */
+    int32_t combine;    /* fs_combine   */
+    int32_t max_batch;  /* largest batch one device pass handles (1..4096) */
+    int32_t device;     /* HIP device ordinal */
+} fs_ensemble_desc;
+
+/* A host image: uint8 HWC RGB, h rows of row_stride bytes (>= 3*w). */
+typedef struct {
+    const uint8_t *data;
+    int32_t h, w, row_stride;
+} fs_image;
+
+/* A device-resident image: offset (bytes) into a packed uint8 buffer. */
+typedef struct {
+    uint64_t offset;
+    int32_t h, w, row_stride, reserved;
+} fs_image_desc;
+
+/* Create an ensemble: validate every model, fold batch norm, convert and
+ * pack the weights, plan every layer for max_batch, allocate one weight
+ * arena and one activation workspace on `device`, upload.
+ * Errors: FS_ERR_INVALID (NULL, inconsistent shapes, unequal class counts),
+ * FS_ERR_UNSUPPORTED (channel counts the kernels do not handle),
+ * FS_ERR_DEVICE (no such device), FS_ERR_OOM. *out is NULL on failure. */
+fs_status fs_ensemble_create(const fs_ensemble_desc *desc, fs_ensemble **out);
+
+/* Ensemble inference over a batch of B host images of any sizes (Sec. 2.3),
+ * synchronous.  B == 0 is a no-op.  B > max_batch is processed in chunks.
+ *   probs      [N][B][C] fp32, required
+ *   mean_probs [B][C]    fp32, optional (NULL)
+ *   vote       [B]       int32, required: smallest c maximising sum_i probs[i][b][c]
+ *   top1       [N][B]    int32, optional: smallest c maximising model i's logits
+ *   logits     [N][B][C] fp32, optional */
+fs_status fs_infer(fs_ensemble *e, const fs_image *imgs, int32_t B,
+                   float *probs, float *mean_probs, int32_t *vote, int32_t *top1,
+                   float *logits);
+
+/* The same pass on device-resident data, asynchronous on `stream`
+ * (a hipStream_t; NULL = the ensemble's own stream).  d_pixels holds the
+ * packed uint8 images, d_desc[B] their descriptors; every output is a
+ * device pointer with the layout of fs_infer (optional ones may be NULL).
+ * Requires 1 <= B <= max_batch.  Nothing is copied to or from the host. */
+fs_status fs_infer_device(fs_ensemble *e, const uint8_t *d_pixels,
+                          const fs_image_desc *d_desc, int32_t B,
+                          float *d_probs, float *d_mean_probs, int32_t *d_vote,
+                          int32_t *d_top1, float *d_logits, void *stream);
+
+void fs_destroy(fs_ensemble *e); /* NULL-safe; waits for outstanding work */
+
+/* Last error message of handle e, or of this thread's last failed create
+ * when e is NULL.  Valid until the next call on the same handle/thread. */
+const char *fs_last_error(const fs_ensemble *e);
+
+typedef struct {
+    int32_t num_models, num_classes, max_batch, precision;
+    int32_t num_groups;          /* launches per layer are shared by a group */
+    int32_t launches_per_pass;   /* kernel launches of one device pass at max_batch */
+    int64_t weight_bytes;        /* device weight arena */
+    int64_t workspace_bytes;     /* device activations + scratch */
+    double flops_per_image;      /* 2 * multiply-accumulates of all models */
+} fs_info;
+fs_status fs_query(const fs_ensemble *e, fs_info *info);
+
+/* Per-kernel-class timing with HIP events on the launch stream.  While
+ * enabled, every launch of fs_infer/fs_infer_device is bracketed by two
+ * events.  fs_profile_read synchronises the stream and returns, per class,
+ * the launch count, summed event time and algorithmic FLOP/bytes. */
+typedef struct {
+    char name[32];
+    int64_t launches;
+    double total_ms;
+    double flops;
+    double bytes;
+} fs_kernel_stat;
+fs_status fs_profile_enable(fs_ensemble *e, int32_t enable); /* (re)starts, clearing */
+fs_status fs_profile_read(fs_ensemble *e, fs_kernel_stat *stats, int32_t max_stats,
+                          int32_t *n_stats);
+
+/* ---- single-kernel entry points on host tensors (synchronous; for parity
+ * tests).  precision selects fp32 or bf16 storage; in bf16 the inputs must
+ * already be bf16-representable and outputs are returned widened to fp32. */
+
+/* Sec. 2.2 transformation of B host images into out [B][out_h][out_w][4]
+ * (channel 3 is zero padding). */
+fs_status fs_test_preprocess(const fs_image *imgs, int32_t B, int32_t out_h, int32_t out_w,
+                             const float mean[3], const float std_[3], int32_t precision,
+                             float *out, int32_t device);
+
+/* Convolution with fused epilogue: out = relu?(conv(in, w) + bias + res).
+ * in [B][H][W][Cin], w [Cout][kh][kw][Cin], bias [Cout] or NULL,
+ * res [B][Ho][Wo][Cout] or NULL, out [B][Ho][Wo][Cout].  tile = -1 picks
+ * the tile the planner would, otherwise forces tile configuration `tile`. */
+fs_status fs_test_conv(const float *in, int32_t B, int32_t H, int32_t W, int32_t Cin,
+                       const float *w, const float *bias, const float *res, int32_t Cout,
+                       int32_t kh, int32_t kw, int32_t stride, int32_t pad, int32_t relu,
+                       int32_t precision, int32_t tile, float *out, int32_t device);
+
+fs_status fs_test_maxpool(const float *in, int32_t B, int32_t H, int32_t W, int32_t C,
+                          int32_t k, int32_t stride, int32_t pad, int32_t precision,
+                          float *out, int32_t device);
+
+fs_status fs_test_gap(const float *in, int32_t B, int32_t H, int32_t W, int32_t C,
+                      int32_t precision, float *out, int32_t device);
+
+/* out [B][N] = relu?(in [B][K] . w[N][K]^T + bias); out_precision selects
+ * an fp32 (final logits) or a storage-type output. */
+fs_status fs_test_fc(const float *in, int32_t B, int32_t K, const float *w, const float *bias,
+                     int32_t N, int32_t relu, int32_t precision, int32_t out_storage,
+                     float *out, int32_t device);
+
+/* Softmax per (model, image) row of logits [N][B][C] and the combination:
+ * probs [N][B][C], mean [B][C] (optional), vote [B], top1 [N][B] (optional). */
+fs_status fs_test_softmax_combine(const float *logits, int32_t N, int32_t B, int32_t C,
+                                  float *probs, float *mean, int32_t *vote, int32_t *top1,
+                                  int32_t device);
+
+/* Number of conv tile configurations fs_test_conv accepts (0..n-1) for a
+ * precision, and the name of tile t (NULL when out of range). */
+int32_t fs_conv_num_tiles(int32_t precision);
+const char *fs_conv_tile_name(int32_t precision, int32_t tile);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLEXSERVE_H */

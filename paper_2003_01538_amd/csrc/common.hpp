@@ -1,0 +1,90 @@
+// Internal declarations shared by the HIP kernels and the host runtime of the
+// ensemble library.  gfx950 (CDNA4) only: 64-lane wavefronts, MFMA, 160 KB LDS.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace fs {
+
+using bf16_t = uint16_t;  // bfloat16 bits in memory
+
+enum Prec { F32 = 0, BF16 = 1 };
+
+// ---------------------------------------------------------------- preprocess
+struct ImageDesc {  // mirrors fs_image_desc
+  uint64_t offset;
+  int32_t h, w, row_stride, reserved;
+};
+
+struct PreArgs {
+  const uint8_t* pixels;
+  const ImageDesc* desc;
+  int B, out_h, out_w;
+  float mean[3], std_[3];
+  void* out;  // [B][out_h][out_w][4], bf16 or fp32
+};
+void launch_preprocess(const PreArgs& a, Prec p, hipStream_t s);
+
+// ---------------------------------------------------------------------- conv
+// Implicit GEMM: rows m = (b, oy, ox), columns n = output channel,
+// reduction k = (ky, kx, ci) with ci fastest.  Z models share a launch; each
+// tensor of model z sits at base + z * mstride (elements).
+struct ConvArgs {
+  const void* x;   int64_t x_mstride;    // [B][H][W][Cin]  (Cin = channel stride)
+  const void* w;   int64_t w_mstride;    // packed [Cout][Kp]
+  const float* bias; int64_t b_mstride;  // [Cout]
+  const void* res; int64_t res_mstride;  // [B][Ho][Wo][Cout] or null
+  void* y;         int64_t y_mstride;    // [B][Ho][Wo][Cout]
+  int B, H, W, Cin, Ho, Wo, Cout;
+  int kh, kw, stride, pad, relu;
+  int K, Kp, M, Z;
+};
+struct ConvTile {
+  int bm, bn, vec;   // block tile and A-load vector (elements)
+  const char* name;
+};
+int conv_num_tiles(Prec p);
+const ConvTile& conv_tile(Prec p, int t);
+int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);
+bool conv_tile_ok(Prec p, int t, const ConvArgs& a);
+void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s);
+constexpr int CONV_KPAD = 64;  // packed reduction length is a multiple of this
+
+// ------------------------------------------------------------------- pooling
+struct PoolArgs {
+  const void* x; int64_t x_mstride;
+  void* y;       int64_t y_mstride;
+  int B, H, W, C, Ho, Wo, k, stride, pad, Z;
+};
+void launch_maxpool(const PoolArgs& a, Prec p, hipStream_t s);
+void launch_gap(const PoolArgs& a, Prec p, hipStream_t s);
+
+// ------------------------------------------------------------------------ fc
+struct FcArgs {
+  const void* x;   int64_t x_mstride;    // [B][K] storage type
+  const void* w;   int64_t w_mstride;    // [N][K] storage type
+  const float* bias; int64_t b_mstride;  // [N]
+  void* y;         int64_t y_mstride;    // [B][N]: fp32 if out_f32 else storage type
+  float* partial;                        // split-K scratch [split][Z][B][N] fp32
+  int B, K, N, relu, out_f32, split, Z;
+};
+int fc_pick_split(Prec p, int B, int K, int N, int Z, int num_cus);
+size_t fc_partial_floats(int B, int N, int split, int Z);
+void launch_fc(const FcArgs& a, Prec p, hipStream_t s);  // 1 or 2 launches (split-K reduce)
+int fc_launches(int split);
+
+// ------------------------------------------------------- softmax + combine
+struct SoftmaxArgs {
+  const float* logits;  // [N][B][C]
+  float* probs;         // [N][B][C]
+  float* mean;          // [B][C] or null
+  int32_t* vote;        // [B]
+  int32_t* top1;        // [N][B] or null
+  int N, B, C;
+};
+constexpr int SOFTMAX_MAX_C = 4096;
+void launch_softmax_combine(const SoftmaxArgs& a, hipStream_t s);
+
+}  // namespace fs

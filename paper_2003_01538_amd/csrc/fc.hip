@@ -1,0 +1,185 @@
+// Fully connected layer y[b][n] = relu?(bias[n] + sum_k x[b][k] * w[n][k]) on
+// the matrix cores.  At serving batch sizes the layer streams its weights
+// once (arithmetic intensity = B FLOP per weight byte), so the kernel is
+// built to keep HBM busy rather than to tile for reuse: every wave owns 16
+// output features, reads its weight rows straight from global memory with
+// 16-byte loads (no LDS; each weight is used by exactly one wave) and
+// multiplies them with 16*FB batch columns per MFMA step.  Large K is split
+// over grid.z (split-K) into an fp32 scratch that a second small kernel sums
+// in a fixed order, so results do not depend on scheduling.
+//
+// MFMA operands: A = 16 weight rows (features), B = 16 batch rows, so each
+// lane's accumulator holds 4 consecutive features of one image.
+#include "common.hpp"
+#include "device.hpp"
+
+#include <algorithm>
+
+namespace fs {
+
+template <int P> struct FcT;
+template <> struct FcT<BF16> { using T = uint16_t; static constexpr int KSTEP = 32; };
+template <> struct FcT<F32> { using T = float; static constexpr int KSTEP = 4; };
+
+constexpr int FC_UNROLL = 4;
+
+template <int P, int FB>
+__global__ void __launch_bounds__(256) k_fc(FcArgs a) {
+  using T = typename FcT<P>::T;
+  constexpr int KSTEP = FcT<P>::KSTEP;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * 64 + wave * 16;
+  const int b0 = blockIdx.y * 16 * FB;
+  const int model = blockIdx.z / a.split, sp = blockIdx.z - model * a.split;
+  const T* __restrict__ x = reinterpret_cast<const T*>(a.x) + model * a.x_mstride;
+  const T* __restrict__ w = reinterpret_cast<const T*>(a.w) + model * a.w_mstride;
+
+  // K range of this split, in whole MFMA steps
+  const int steps = (a.K + KSTEP - 1) / KSTEP;
+  const int per = (steps + a.split - 1) / a.split;
+  const int kb = sp * per * KSTEP;
+  const int ke = min(a.K, kb + per * KSTEP);
+
+  const int row_n = n0 + (lane & 15);
+  const bool n_ok = row_n < a.N;
+  constexpr int LE = P == BF16 ? 8 : 1;  // elements per lane per step
+  const int koff = (lane >> 4) * LE;
+  const T* wrow = w + (int64_t)(n_ok ? row_n : 0) * a.K + koff;
+  const T* xrow[FB];
+  bool b_ok[FB];
+#pragma unroll
+  for (int f = 0; f < FB; ++f) {
+    int bb = b0 + f * 16 + (lane & 15);
+    b_ok[f] = bb < a.B;
+    xrow[f] = x + (int64_t)(b_ok[f] ? bb : 0) * a.K + koff;
+  }
+
+  floatx4 acc[FB];
+#pragma unroll
+  for (int f = 0; f < FB; ++f) acc[f] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k = kb; k < ke; k += KSTEP * FC_UNROLL) {
+    if constexpr (P == BF16) {
+      uint4 wa[FC_UNROLL], xb[FC_UNROLL][FB];
+#pragma unroll
+      for (int u = 0; u < FC_UNROLL; ++u) {
+        const int kk = k + u * KSTEP + koff;
+        const bool kin = kk + LE <= ke;
+        wa[u] = (kin && n_ok) ? *reinterpret_cast<const uint4*>(wrow + k + u * KSTEP) : uint4{0, 0, 0, 0};
+#pragma unroll
+        for (int f = 0; f < FB; ++f)
+          xb[u][f] = (kin && b_ok[f]) ? *reinterpret_cast<const uint4*>(xrow[f] + k + u * KSTEP)
+                                      : uint4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int u = 0; u < FC_UNROLL; ++u)
+#pragma unroll
+        for (int f = 0; f < FB; ++f)
+          acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[u]),
+                                                           __builtin_bit_cast(bf16x8, xb[u][f]),
+                                                           acc[f], 0, 0, 0);
+    } else {
+      float wa[FC_UNROLL], xb[FC_UNROLL][FB];
+#pragma unroll
+      for (int u = 0; u < FC_UNROLL; ++u) {
+        const int kk = k + u * KSTEP + koff;
+        const bool kin = kk < ke;
+        wa[u] = (kin && n_ok) ? wrow[k + u * KSTEP] : 0.f;
+#pragma unroll
+        for (int f = 0; f < FB; ++f) xb[u][f] = (kin && b_ok[f]) ? xrow[f][k + u * KSTEP] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < FC_UNROLL; ++u)
+#pragma unroll
+        for (int f = 0; f < FB; ++f)
+          acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[u], xb[u][f], acc[f], 0, 0, 0);
+    }
+  }
+
+  // acc[f][r] = y[b = b0 + 16f + (lane & 15)][n = n0 + 4 (lane >> 4) + r]
+  const float* bias = a.bias + model * a.b_mstride;
+#pragma unroll
+  for (int f = 0; f < FB; ++f) {
+    const int bb = b0 + f * 16 + (lane & 15);
+    if (bb >= a.B) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int n = n0 + (lane >> 4) * 4 + r;
+      if (n >= a.N) continue;
+      if (a.split > 1) {
+        a.partial[(((int64_t)sp * a.Z + model) * a.B + bb) * a.N + n] = acc[f][r];
+      } else {
+        float v = acc[f][r] + bias[n];
+        if (a.relu) v = fmaxf(v, 0.f);
+        const int64_t o = (int64_t)bb * a.N + n;
+        if (a.out_f32 || P == F32)
+          (reinterpret_cast<float*>(a.y) + model * a.y_mstride)[o] = v;
+        else
+          (reinterpret_cast<uint16_t*>(a.y) + model * a.y_mstride)[o] = f2bf(v);
+      }
+    }
+  }
+}
+
+// Sum of the split-K partials in split order, then bias, ReLU and the store.
+__global__ void __launch_bounds__(256) k_fc_reduce(FcArgs a, int out_bf16) {
+  const int64_t total = (int64_t)a.Z * a.B * a.N;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int n = (int)(i % a.N);
+  const int64_t t = i / a.N;
+  const int bb = (int)(t % a.B), model = (int)(t / a.B);
+  float v = 0.f;
+  for (int sp = 0; sp < a.split; ++sp)
+    v += a.partial[(((int64_t)sp * a.Z + model) * a.B + bb) * a.N + n];
+  v += a.bias[model * a.b_mstride + n];
+  if (a.relu) v = fmaxf(v, 0.f);
+  const int64_t o = (int64_t)bb * a.N + n;
+  if (out_bf16)
+    (reinterpret_cast<uint16_t*>(a.y) + model * a.y_mstride)[o] = f2bf(v);
+  else
+    (reinterpret_cast<float*>(a.y) + model * a.y_mstride)[o] = v;
+}
+
+static int fc_fb(int B) { return B > 32 ? 4 : (B > 16 ? 2 : 1); }
+
+int fc_pick_split(Prec p, int B, int K, int N, int Z, int num_cus) {
+  const int fb = fc_fb(B);
+  const int wgs = ((N + 63) / 64) * ((B + 16 * fb - 1) / (16 * fb)) * Z;
+  const int kstep = p == BF16 ? 32 : 4;
+  const int max_split = std::max(1, K / (kstep * FC_UNROLL * 4));  // >= 4 unrolled steps per split
+  int split = (2 * num_cus + wgs - 1) / wgs;
+  return std::max(1, std::min(split, std::min(max_split, 32)));
+}
+
+size_t fc_partial_floats(int B, int N, int split, int Z) {
+  return split > 1 ? (size_t)split * Z * B * N : 0;
+}
+
+int fc_launches(int split) { return split > 1 ? 2 : 1; }
+
+template <int P, int FB>
+static void launch_fc_t(const FcArgs& a, hipStream_t s) {
+  dim3 grid((a.N + 63) / 64, (a.B + 16 * FB - 1) / (16 * FB), a.split * a.Z);
+  hipLaunchKernelGGL((k_fc<P, FB>), grid, dim3(256), 0, s, a);
+}
+
+void launch_fc(const FcArgs& a, Prec p, hipStream_t s) {
+  const int fb = fc_fb(a.B);
+  if (p == BF16) {
+    if (fb == 4) launch_fc_t<BF16, 4>(a, s);
+    else if (fb == 2) launch_fc_t<BF16, 2>(a, s);
+    else launch_fc_t<BF16, 1>(a, s);
+  } else {
+    if (fb == 4) launch_fc_t<F32, 4>(a, s);
+    else if (fb == 2) launch_fc_t<F32, 2>(a, s);
+    else launch_fc_t<F32, 1>(a, s);
+  }
+  if (a.split > 1) {
+    const int64_t total = (int64_t)a.Z * a.B * a.N;
+    const int out_bf16 = (p == BF16 && !a.out_f32) ? 1 : 0;
+    hipLaunchKernelGGL(k_fc_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a, out_bf16);
+  }
+}
+
+}  // namespace fs

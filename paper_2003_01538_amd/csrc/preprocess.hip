@@ -1,0 +1,66 @@
+// The one data transformation shared by every model of the ensemble
+// (FlexServe, Fig. 1 caption; Sec. 2.2): bilinear resize of each uint8 HWC
+// image to out_h x out_w (half-pixel centres, no antialias, the upper
+// neighbour clamped at the border), then (v/255 - mean)/std per channel,
+// written once as NHWC with the channel dimension padded to 4 (the padding
+// channel is 0) so that the first convolution loads one aligned 8- or
+// 16-byte vector per pixel.
+//
+// One thread per output pixel, 256 consecutive pixels of one image per
+// workgroup: the stores are fully coalesced; the four taps are gathered
+// through the cache (HBM-bound on the output for upscaling, on the input for
+// downscaling).  Ragged batches need no host work: each image's size comes
+// from its device-side descriptor.
+#include "common.hpp"
+#include "device.hpp"
+
+namespace fs {
+
+template <bool BF16>
+__global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
+  const int b = blockIdx.y;
+  const int pix = blockIdx.x * 256 + threadIdx.x;
+  if (pix >= a.out_h * a.out_w) return;
+  const int oy = pix / a.out_w, ox = pix - oy * a.out_w;
+  const ImageDesc d = a.desc[b];
+  const uint8_t* img = a.pixels + d.offset;
+
+  const float sh = (float)d.h / (float)a.out_h;
+  const float sw = (float)d.w / (float)a.out_w;
+  float sy = fmaxf(((float)oy + 0.5f) * sh - 0.5f, 0.0f);
+  float sx = fmaxf(((float)ox + 0.5f) * sw - 0.5f, 0.0f);
+  int y0 = min((int)sy, d.h - 1), x0 = min((int)sx, d.w - 1);
+  int y1 = min(y0 + 1, d.h - 1), x1 = min(x0 + 1, d.w - 1);
+  float ly = sy - (float)y0, lx = sx - (float)x0;
+  float hy = 1.0f - ly, hx = 1.0f - lx;
+
+  const uint8_t* r0 = img + (int64_t)y0 * d.row_stride;
+  const uint8_t* r1 = img + (int64_t)y1 * d.row_stride;
+  float o[4];
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    float v00 = r0[x0 * 3 + c], v01 = r0[x1 * 3 + c];
+    float v10 = r1[x0 * 3 + c], v11 = r1[x1 * 3 + c];
+    float v = hy * (hx * v00 + lx * v01) + ly * (hx * v10 + lx * v11);
+    o[c] = (v / 255.0f - a.mean[c]) / a.std_[c];
+  }
+  o[3] = 0.0f;
+  const int64_t idx = ((int64_t)b * a.out_h * a.out_w + pix);
+  if (BF16) {
+    floatx4 f = {o[0], o[1], o[2], o[3]};
+    bf16x4 h = __builtin_convertvector(f, bf16x4);
+    reinterpret_cast<uint2*>(a.out)[idx] = __builtin_bit_cast(uint2, h);
+  } else {
+    reinterpret_cast<float4*>(a.out)[idx] = make_float4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+void launch_preprocess(const PreArgs& a, Prec p, hipStream_t s) {
+  dim3 grid((a.out_h * a.out_w + 255) / 256, a.B);
+  if (p == BF16)
+    hipLaunchKernelGGL(k_preprocess<true>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_preprocess<false>, grid, dim3(256), 0, s, a);
+}
+
+}  // namespace fs

@@ -1,0 +1,1113 @@
+// Host runtime behind the C ABI: validation, weight preparation (batch-norm
+// fold, packing, bf16 conversion, one weight arena), the ensemble plan
+// (homogeneous models grouped so one launch per layer serves all of them,
+// activation slots reused by liveness), the device pass, host staging, and
+// the per-kernel event profiler.
+//
+// FlexServe (Fig. 1 caption; Sec. 2.2): all models live in one device memory
+// and consume ONE transformed copy of the request's images; the batch size
+// varies per request (Sec. 2.3); every model's per-image output is returned
+// together with a combined result.
+#include "flexserve.h"
+#include "common.hpp"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+namespace {
+
+using namespace fs;
+
+struct Error {
+  fs_status st;
+  std::string msg;
+};
+[[noreturn]] void fail(fs_status st, const std::string& msg) { throw Error{st, msg}; }
+
+void hipchk(hipError_t e, const char* what) {
+  if (e == hipSuccess) return;
+  fail(e == hipErrorOutOfMemory ? FS_ERR_OOM : FS_ERR_DEVICE,
+       std::string(what) + ": " + hipGetErrorString(e));
+}
+#define HIPCHK(x) hipchk((x), #x)
+
+thread_local std::string g_thread_error;
+
+// Round to nearest even fp32 -> bf16 on the host (weights).
+uint16_t host_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (u & 0x007fffffu) ? uint16_t((u >> 16) | 0x40) : uint16_t(u >> 16);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+float host_bf16_to_f(uint16_t h) {
+  uint32_t u = uint32_t(h) << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ------------------------------------------------------------ device memory
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  void alloc(size_t n) {
+    release();
+    if (n == 0) return;
+    HIPCHK(hipMalloc(&p, n));
+    bytes = n;
+  }
+  void ensure(size_t n) {
+    if (n > bytes) alloc(n);
+  }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    bytes = 0;
+  }
+  ~DevBuf() { release(); }
+};
+
+struct HostBuf {  // pinned
+  void* p = nullptr;
+  size_t bytes = 0;
+  void ensure(size_t n) {
+    if (n <= bytes) return;
+    release();
+    HIPCHK(hipHostMalloc(&p, n, hipHostMallocDefault));
+    bytes = n;
+  }
+  void release() {
+    if (p) (void)hipHostFree(p);
+    p = nullptr;
+    bytes = 0;
+  }
+  ~HostBuf() { release(); }
+};
+
+// ------------------------------------------------------------------- plan
+struct Shape {
+  int H = 0, W = 0, C = 0;
+  int64_t elems() const { return (int64_t)H * W * C; }
+};
+
+enum { SLOT_INPUT = -2, SLOT_LOGITS = -3 };
+
+struct LayerPlan {
+  int op = 0, src = -1, res = -1;
+  Shape in, out;
+  int cin_p = 0;  // channel stride of the input tensor
+  int kh = 1, kw = 1, stride = 1, pad = 0, relu = 0, flatten = 0;
+  int K = 0, Kp = 0;
+  size_t w_off = 0, b_off = 0;  // bytes into the arena (model 0)
+  int64_t w_melems = 0, b_melems = 0;
+  int in_slot = SLOT_INPUT, res_slot = -1, out_slot = -1;
+  bool last = false;
+};
+
+struct Group {
+  int first = 0, Z = 1;
+  std::vector<LayerPlan> layers;
+  std::vector<int64_t> slot_elems;  // per image, per model
+  std::vector<DevBuf> slots;        // [Z][max_batch][slot_elems]
+};
+
+enum KClass { K_PRE = 0, K_CONV, K_MAXPOOL, K_GAP, K_FC, K_SOFTMAX, K_NCLASS };
+const char* kClassName[K_NCLASS] = {"preprocess", "conv", "maxpool", "gap", "fc", "softmax_combine"};
+
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+  double flops, bytes;
+  int launches;
+};
+
+}  // namespace
+
+struct fs_ensemble {
+  std::mutex mu;
+  std::string err;
+  int device = 0, num_cus = 256;
+  Prec prec = BF16;
+  int N = 0, C = 0, max_batch = 0;
+  fs_preprocess pre{};
+  std::vector<Group> groups;
+  double flops_per_image = 0;
+  DevBuf arena;
+  size_t arena_bytes = 0;
+  DevBuf input;     // [max_batch][out_h][out_w][4]
+  DevBuf partial;   // fc split-K scratch
+  DevBuf logits;    // [N][max_batch][C] fp32
+  // host-path staging
+  DevBuf d_pixels, d_desc, d_probs, d_mean, d_vote, d_top1;
+  HostBuf h_pixels, h_desc, h_out;
+  hipStream_t stream = nullptr;
+  // profiler
+  bool prof_on = false;
+  std::vector<ProfRec> prof;
+  std::vector<hipEvent_t> ev_pool;
+  int64_t workspace_bytes = 0;
+};
+
+namespace {
+
+size_t es(Prec p) { return p == BF16 ? 2 : 4; }
+
+// ----------------------------------------------------------- validation
+void validate_desc(const fs_ensemble_desc* d) {
+  if (!d) fail(FS_ERR_INVALID, "desc is NULL");
+  if (d->num_models < 1 || !d->models) fail(FS_ERR_INVALID, "num_models must be >= 1 with a models array");
+  if (d->precision != FS_F32 && d->precision != FS_BF16) fail(FS_ERR_INVALID, "precision must be FS_F32 or FS_BF16");
+  if (d->combine != FS_COMBINE_MEAN) fail(FS_ERR_UNSUPPORTED, "only FS_COMBINE_MEAN is supported");
+  if (d->max_batch < 1 || d->max_batch > 4096) fail(FS_ERR_INVALID, "max_batch must be in 1..4096");
+  if (d->pre.out_h < 1 || d->pre.out_w < 1 || d->pre.out_h > 4096 || d->pre.out_w > 4096)
+    fail(FS_ERR_INVALID, "preprocess output size must be in 1..4096");
+  for (int c = 0; c < 3; ++c)
+    if (!std::isfinite(d->pre.mean[c]) || !std::isfinite(d->pre.std[c]) || d->pre.std[c] == 0.f)
+      fail(FS_ERR_INVALID, "mean/std must be finite and std non-zero");
+  const int prec = d->precision;
+  const int C = d->models[0].num_classes;
+  for (int m = 0; m < d->num_models; ++m) {
+    const fs_model_spec& s = d->models[m];
+    const std::string pfx = "model " + std::to_string(m) + ": ";
+    if (s.num_layers < 1 || !s.layers) fail(FS_ERR_INVALID, pfx + "no layers");
+    if (s.num_classes < 1) fail(FS_ERR_INVALID, pfx + "num_classes must be >= 1");
+    if (s.num_classes != C) fail(FS_ERR_INVALID, pfx + "num_classes differs between models (the combine needs one class set)");
+    if (s.num_classes > SOFTMAX_MAX_C) fail(FS_ERR_UNSUPPORTED, pfx + "more than 4096 classes");
+    std::vector<Shape> out(s.num_layers);
+    for (int i = 0; i < s.num_layers; ++i) {
+      const fs_layer& L = s.layers[i];
+      const std::string lp = pfx + "layer " + std::to_string(i) + ": ";
+      if (L.src < -1 || L.src >= i) fail(FS_ERR_INVALID, lp + "src must be -1 or an earlier layer");
+      Shape in = L.src < 0 ? Shape{d->pre.out_h, d->pre.out_w, 3} : out[L.src];
+      const bool last = i == s.num_layers - 1;
+      switch (L.op) {
+        case FS_OP_CONV: {
+          if (!L.weight) fail(FS_ERR_INVALID, lp + "conv weight is NULL");
+          if (L.cin != in.C) fail(FS_ERR_INVALID, lp + "conv cin does not match its input channels");
+          if (L.cout < 1 || L.kh < 1 || L.kw < 1 || L.stride < 1 || L.pad < 0)
+            fail(FS_ERR_INVALID, lp + "conv geometry");
+          int Ho = (in.H + 2 * L.pad - L.kh) / L.stride + 1, Wo = (in.W + 2 * L.pad - L.kw) / L.stride + 1;
+          if (in.H + 2 * L.pad < L.kh || in.W + 2 * L.pad < L.kw || Ho < 1 || Wo < 1)
+            fail(FS_ERR_INVALID, lp + "conv output would be empty");
+          if (L.cout % 8) fail(FS_ERR_UNSUPPORTED, lp + "conv cout must be a multiple of 8");
+          if (L.src >= 0 && L.cin % 8) fail(FS_ERR_UNSUPPORTED, lp + "conv cin must be a multiple of 8");
+          out[i] = Shape{Ho, Wo, L.cout};
+          if (L.residual_src != -1) {
+            if (L.residual_src < 0 || L.residual_src >= i) fail(FS_ERR_INVALID, lp + "residual_src must be -1 or an earlier layer");
+            const Shape& r = out[L.residual_src];
+            if (r.H != Ho || r.W != Wo || r.C != L.cout) fail(FS_ERR_INVALID, lp + "residual shape differs from the conv output");
+          }
+          if (last) fail(FS_ERR_INVALID, lp + "the last layer must be fc");
+          break;
+        }
+        case FS_OP_MAXPOOL: {
+          if (L.src < 0) fail(FS_ERR_UNSUPPORTED, lp + "max pool directly on the transformed input");
+          if (L.kh < 1 || L.kh != L.kw || L.stride < 1 || L.pad < 0 || L.pad >= L.kh)
+            fail(FS_ERR_INVALID, lp + "max pool geometry (square window, 0 <= pad < k)");
+          int Ho = (in.H + 2 * L.pad - L.kh) / L.stride + 1, Wo = (in.W + 2 * L.pad - L.kw) / L.stride + 1;
+          if (in.H + 2 * L.pad < L.kh || in.W + 2 * L.pad < L.kw || Ho < 1 || Wo < 1)
+            fail(FS_ERR_INVALID, lp + "max pool output would be empty");
+          out[i] = Shape{Ho, Wo, in.C};
+          if (last) fail(FS_ERR_INVALID, lp + "the last layer must be fc");
+          break;
+        }
+        case FS_OP_GAP:
+          if (L.src < 0) fail(FS_ERR_UNSUPPORTED, lp + "global pool directly on the transformed input");
+          out[i] = Shape{1, 1, in.C};
+          if (last) fail(FS_ERR_INVALID, lp + "the last layer must be fc");
+          break;
+        case FS_OP_FC: {
+          if (L.src < 0) fail(FS_ERR_UNSUPPORTED, lp + "fc directly on the transformed input");
+          if (!L.weight) fail(FS_ERR_INVALID, lp + "fc weight is NULL");
+          if ((int64_t)L.cin != in.elems()) fail(FS_ERR_INVALID, lp + "fc cin does not match the flattened input");
+          if (L.cout < 1) fail(FS_ERR_INVALID, lp + "fc cout must be >= 1");
+          if (prec == FS_BF16 && L.cin % 8) fail(FS_ERR_UNSUPPORTED, lp + "bf16 fc cin must be a multiple of 8");
+          if (!last && L.cout % 8) fail(FS_ERR_UNSUPPORTED, lp + "hidden fc cout must be a multiple of 8");
+          if (last && L.cout != s.num_classes) fail(FS_ERR_INVALID, lp + "last fc cout differs from num_classes");
+          out[i] = Shape{1, 1, L.cout};
+          break;
+        }
+        default:
+          fail(FS_ERR_INVALID, lp + "unknown op");
+      }
+      if (out[i].elems() * (int64_t)d->max_batch >= (int64_t(1) << 31))
+        fail(FS_ERR_UNSUPPORTED, lp + "activation tensor too large for max_batch (2^31 elements)");
+    }
+    if (s.layers[s.num_layers - 1].op != FS_OP_FC) fail(FS_ERR_INVALID, pfx + "the last layer must be fc");
+  }
+  if ((int64_t)d->pre.out_h * d->pre.out_w * 4 * d->max_batch >= (int64_t(1) << 31))
+    fail(FS_ERR_UNSUPPORTED, "transformed input too large for max_batch");
+}
+
+bool same_structure(const fs_model_spec& a, const fs_model_spec& b) {
+  if (a.num_layers != b.num_layers) return false;
+  for (int i = 0; i < a.num_layers; ++i) {
+    const fs_layer &x = a.layers[i], &y = b.layers[i];
+    if (x.op != y.op || x.src != y.src || x.residual_src != y.residual_src || x.cin != y.cin ||
+        x.cout != y.cout || x.kh != y.kh || x.kw != y.kw || x.stride != y.stride || x.pad != y.pad ||
+        x.relu != y.relu || x.flatten_nchw != y.flatten_nchw)
+      return false;
+  }
+  return true;
+}
+
+// ------------------------------------------------------- weight packing
+// conv: [Cout][kh][kw][cin] (fp32, BN folded here) -> [Cout][Kp] with
+// k = (ky*kw + kx)*cin_p + ci, zeros in padded positions.
+void pack_conv(const fs_layer& L, int cin_p, int Kp, Prec p, void* dst_w, float* dst_b) {
+  const int taps = L.kh * L.kw;
+  for (int co = 0; co < L.cout; ++co) {
+    const float s = L.bn_scale ? L.bn_scale[co] : 1.0f;
+    for (int k = 0; k < Kp; ++k) {
+      float v = 0.f;
+      const int tap = k / cin_p, ci = k % cin_p;
+      if (tap < taps && ci < L.cin) {
+        v = L.weight[((int64_t)co * taps + tap) * L.cin + ci];
+        if (L.bn_scale) v = v * s;
+      }
+      if (p == BF16)
+        static_cast<uint16_t*>(dst_w)[(int64_t)co * Kp + k] = host_bf16(v);
+      else
+        static_cast<float*>(dst_w)[(int64_t)co * Kp + k] = v;
+    }
+    dst_b[co] = L.bn_shift ? L.bn_shift[co] : (L.bias ? L.bias[co] : 0.f);
+  }
+}
+
+// fc: [N][K]; with flatten_nchw the columns are permuted from the
+// channel-major order c*H*W + y*W + x to the NHWC order (y*W + x)*C + c.
+void pack_fc(const fs_layer& L, const Shape& in, Prec p, void* dst_w, float* dst_b) {
+  const int K = L.cin, HW = in.H * in.W;
+  for (int n = 0; n < L.cout; ++n) {
+    for (int k = 0; k < K; ++k) {
+      int src_k = k;
+      if (L.flatten_nchw) {
+        const int pix = k / in.C, c = k % in.C;
+        src_k = c * HW + pix;
+      }
+      const float v = L.weight[(int64_t)n * K + src_k];
+      if (p == BF16)
+        static_cast<uint16_t*>(dst_w)[(int64_t)n * K + k] = host_bf16(v);
+      else
+        static_cast<float*>(dst_w)[(int64_t)n * K + k] = v;
+    }
+    dst_b[n] = L.bias ? L.bias[n] : 0.f;
+  }
+}
+
+// ----------------------------------------------------------- planning
+void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
+  const fs_model_spec& s = d->models[g.first];
+  const int n = s.num_layers;
+  g.layers.resize(n);
+  std::vector<Shape> out(n);
+  std::vector<int> last_use(n, -1);
+  for (int i = 0; i < n; ++i) {
+    const fs_layer& L = s.layers[i];
+    if (L.src >= 0) last_use[L.src] = std::max(last_use[L.src], i);
+    if (L.op == FS_OP_CONV && L.residual_src >= 0) last_use[L.residual_src] = std::max(last_use[L.residual_src], i);
+  }
+  // slots: greedy reuse of freed buffers
+  std::vector<int> slot_busy_until;  // layer index of last reader, per slot
+  std::vector<int64_t>& slot_elems = g.slot_elems;
+  std::vector<int> layer_slot(n, -1);
+  for (int i = 0; i < n; ++i) {
+    const fs_layer& L = s.layers[i];
+    LayerPlan& P = g.layers[i];
+    P.op = L.op;
+    P.src = L.src;
+    P.res = L.op == FS_OP_CONV ? L.residual_src : -1;
+    P.in = L.src < 0 ? Shape{d->pre.out_h, d->pre.out_w, 3} : out[L.src];
+    P.cin_p = L.src < 0 ? 4 : P.in.C;
+    P.kh = L.kh; P.kw = L.kw; P.stride = L.stride; P.pad = L.pad;
+    P.relu = L.relu ? 1 : 0;
+    P.flatten = L.flatten_nchw ? 1 : 0;
+    P.last = i == n - 1;
+    switch (L.op) {
+      case FS_OP_CONV:
+        P.out = Shape{(P.in.H + 2 * L.pad - L.kh) / L.stride + 1, (P.in.W + 2 * L.pad - L.kw) / L.stride + 1, L.cout};
+        P.K = L.kh * L.kw * P.cin_p;
+        P.Kp = (int)round_up(P.K, CONV_KPAD);
+        e->flops_per_image += 2.0 * P.out.H * P.out.W * L.cout * (double)L.kh * L.kw * L.cin * g.Z;
+        break;
+      case FS_OP_MAXPOOL:
+        P.out = Shape{(P.in.H + 2 * L.pad - L.kh) / L.stride + 1, (P.in.W + 2 * L.pad - L.kw) / L.stride + 1, P.in.C};
+        break;
+      case FS_OP_GAP:
+        P.out = Shape{1, 1, P.in.C};
+        break;
+      case FS_OP_FC:
+        P.out = Shape{1, 1, L.cout};
+        P.K = L.cin;
+        e->flops_per_image += 2.0 * L.cin * L.cout * g.Z;
+        break;
+    }
+    out[i] = P.out;
+    P.in_slot = L.src < 0 ? SLOT_INPUT : layer_slot[L.src];
+    P.res_slot = P.res >= 0 ? layer_slot[P.res] : -1;
+    // free slots whose readers are all at or before this layer... but not
+    // before this layer has read them: release after assigning the output.
+    if (P.last) {
+      P.out_slot = SLOT_LOGITS;
+    } else {
+      const int64_t need = P.out.elems();
+      int pick = -1;
+      for (size_t sidx = 0; sidx < slot_busy_until.size(); ++sidx) {
+        if (slot_busy_until[sidx] < i) {  // free: its last reader ran before layer i
+          if (pick < 0 || std::llabs(slot_elems[sidx] - need) < std::llabs(slot_elems[pick] - need)) pick = (int)sidx;
+        }
+      }
+      if (pick < 0) {
+        slot_elems.push_back(need);
+        slot_busy_until.push_back(0);
+        pick = (int)slot_elems.size() - 1;
+      }
+      slot_elems[pick] = std::max(slot_elems[pick], need);
+      slot_busy_until[pick] = std::max(last_use[i], i);
+      layer_slot[i] = pick;
+      P.out_slot = pick;
+    }
+  }
+}
+
+int num_cus_of(int dev) {
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  return n;
+}
+
+void set_device(int dev) {
+  int count = 0;
+  hipError_t err = hipGetDeviceCount(&count);
+  if (err != hipSuccess || count <= 0) fail(FS_ERR_DEVICE, std::string("no HIP device available: ") + hipGetErrorString(err));
+  if (dev < 0 || dev >= count) fail(FS_ERR_DEVICE, "device ordinal " + std::to_string(dev) + " out of range");
+  HIPCHK(hipSetDevice(dev));
+}
+
+void build(fs_ensemble* e, const fs_ensemble_desc* d) {
+  e->prec = d->precision == FS_BF16 ? BF16 : F32;
+  e->N = d->num_models;
+  e->C = d->models[0].num_classes;
+  e->max_batch = d->max_batch;
+  e->pre = d->pre;
+  e->device = d->device;
+  // groups of consecutive structurally identical models
+  for (int m = 0; m < e->N;) {
+    int z = 1;
+    while (m + z < e->N && same_structure(d->models[m], d->models[m + z])) ++z;
+    Group g;
+    g.first = m;
+    g.Z = z;
+    e->groups.push_back(std::move(g));
+    m += z;
+  }
+  for (Group& g : e->groups) plan_group(e, d, g);
+
+  // weight arena layout
+  const size_t esz = es(e->prec);
+  size_t off = 0;
+  for (Group& g : e->groups) {
+    for (LayerPlan& P : g.layers) {
+      if (P.op == FS_OP_CONV || P.op == FS_OP_FC) {
+        const int64_t welems = P.op == FS_OP_CONV ? (int64_t)P.out.C * P.Kp : (int64_t)P.out.C * P.K;
+        P.w_melems = (int64_t)round_up(welems, 128);
+        P.b_melems = (int64_t)round_up(P.out.C, 64);
+        P.w_off = off;
+        off += (size_t)P.w_melems * esz * g.Z;
+        P.b_off = off;
+        off += (size_t)P.b_melems * 4 * g.Z;
+        off = round_up(off, 256);
+      }
+    }
+  }
+  e->arena_bytes = off;
+  std::vector<char> host(off, 0);
+  for (Group& g : e->groups) {
+    for (int li = 0; li < (int)g.layers.size(); ++li) {
+      LayerPlan& P = g.layers[li];
+      if (P.op != FS_OP_CONV && P.op != FS_OP_FC) continue;
+      for (int z = 0; z < g.Z; ++z) {
+        const fs_layer& L = d->models[g.first + z].layers[li];
+        void* wdst = host.data() + P.w_off + (size_t)z * P.w_melems * esz;
+        float* bdst = reinterpret_cast<float*>(host.data() + P.b_off + (size_t)z * P.b_melems * 4);
+        if (P.op == FS_OP_CONV)
+          pack_conv(L, P.cin_p, P.Kp, e->prec, wdst, bdst);
+        else
+          pack_fc(L, P.in, e->prec, wdst, bdst);
+      }
+    }
+  }
+
+  set_device(e->device);
+  e->num_cus = num_cus_of(e->device);
+  HIPCHK(hipStreamCreateWithFlags(&e->stream, hipStreamNonBlocking));
+  e->arena.alloc(std::max<size_t>(off, 256));
+  HIPCHK(hipMemcpy(e->arena.p, host.data(), off, hipMemcpyHostToDevice));
+
+  const int Bm = e->max_batch;
+  int64_t ws = 0;
+  for (Group& g : e->groups) {
+    g.slots.resize(g.slot_elems.size());
+    for (size_t sidx = 0; sidx < g.slot_elems.size(); ++sidx) {
+      const size_t bytes = round_up((size_t)g.slot_elems[sidx] * Bm * g.Z * esz, 256);
+      g.slots[sidx].alloc(bytes);
+      ws += bytes;
+    }
+  }
+  // split-K scratch of the FC layers: the split depends on B, so size it
+  // for the worst case over every batch size a pass can see
+  size_t pf_all = 0;
+  for (Group& g : e->groups)
+    for (LayerPlan& P : g.layers)
+      if (P.op == FS_OP_FC)
+        for (int B = 1; B <= Bm; ++B)
+          pf_all = std::max(pf_all, fc_partial_floats(B, P.out.C, fc_pick_split(e->prec, B, P.K, P.out.C, g.Z, e->num_cus), g.Z));
+  e->partial.alloc(round_up(std::max<size_t>(pf_all, 1) * 4, 256));
+  e->input.alloc(round_up((size_t)Bm * e->pre.out_h * e->pre.out_w * 4 * esz, 256));
+  e->logits.alloc(round_up((size_t)e->N * Bm * e->C * 4, 256));
+  ws += e->partial.bytes + e->input.bytes + e->logits.bytes;
+  e->workspace_bytes = ws;
+}
+
+// ------------------------------------------------------------- profiler
+struct Launcher {
+  fs_ensemble* e;
+  hipStream_t s;
+  template <class F>
+  void operator()(int cls, double flops, double bytes, int launches, F&& fn) {
+    if (!e->prof_on) {
+      fn();
+      return;
+    }
+    auto take = [&]() {
+      hipEvent_t ev;
+      if (!e->ev_pool.empty()) {
+        ev = e->ev_pool.back();
+        e->ev_pool.pop_back();
+      } else {
+        HIPCHK(hipEventCreate(&ev));
+      }
+      return ev;
+    };
+    ProfRec r{cls, take(), take(), flops, bytes, launches};
+    HIPCHK(hipEventRecord(r.a, s));
+    fn();
+    HIPCHK(hipEventRecord(r.b, s));
+    e->prof.push_back(r);
+  }
+};
+
+void prof_clear(fs_ensemble* e) {
+  for (ProfRec& r : e->prof) {
+    e->ev_pool.push_back(r.a);
+    e->ev_pool.push_back(r.b);
+  }
+  e->prof.clear();
+}
+
+// ------------------------------------------------------------ device pass
+void* slot_ptr(Group& g, int slot) { return g.slots[slot].p; }
+
+void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
+              float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s) {
+  Launcher launch{e, s};
+  const Prec p = e->prec;
+  const size_t esz = es(p);
+  const int oh = e->pre.out_h, ow = e->pre.out_w;
+  const int Bm = e->max_batch;
+  float* logits = d_logits ? d_logits : static_cast<float*>(e->logits.p);
+
+  PreArgs pa{};
+  pa.pixels = d_pixels;
+  pa.desc = d_desc;
+  pa.B = B;
+  pa.out_h = oh;
+  pa.out_w = ow;
+  for (int c = 0; c < 3; ++c) {
+    pa.mean[c] = e->pre.mean[c];
+    pa.std_[c] = e->pre.std[c];
+  }
+  pa.out = e->input.p;
+  launch(K_PRE, 0.0, (double)B * oh * ow * 3 * esz, 1, [&] { launch_preprocess(pa, p, s); });
+
+  char* arena = static_cast<char*>(e->arena.p);
+  for (Group& g : e->groups) {
+    for (LayerPlan& P : g.layers) {
+      const void* x = P.in_slot == SLOT_INPUT ? e->input.p : slot_ptr(g, P.in_slot);
+      const int64_t x_ms = P.in_slot == SLOT_INPUT ? 0 : (int64_t)g.slot_elems[P.in_slot] * Bm;
+      void* y = nullptr;
+      int64_t y_ms = 0;
+      if (P.out_slot == SLOT_LOGITS) {
+        y = logits + (int64_t)g.first * B * e->C;
+        y_ms = (int64_t)B * e->C;
+      } else {
+        y = slot_ptr(g, P.out_slot);
+        y_ms = (int64_t)g.slot_elems[P.out_slot] * Bm;
+      }
+      switch (P.op) {
+        case FS_OP_CONV: {
+          ConvArgs a{};
+          a.x = x; a.x_mstride = x_ms;
+          a.w = arena + P.w_off; a.w_mstride = P.w_melems;
+          a.bias = reinterpret_cast<const float*>(arena + P.b_off); a.b_mstride = P.b_melems;
+          a.res = P.res_slot >= 0 ? slot_ptr(g, P.res_slot) : nullptr;
+          a.res_mstride = P.res_slot >= 0 ? (int64_t)g.slot_elems[P.res_slot] * Bm : 0;
+          a.y = y; a.y_mstride = y_ms;
+          a.B = B; a.H = P.in.H; a.W = P.in.W; a.Cin = P.cin_p;
+          a.Ho = P.out.H; a.Wo = P.out.W; a.Cout = P.out.C;
+          a.kh = P.kh; a.kw = P.kw; a.stride = P.stride; a.pad = P.pad; a.relu = P.relu;
+          a.K = P.K; a.Kp = P.Kp; a.M = B * P.out.H * P.out.W; a.Z = g.Z;
+          const int tile = conv_pick_tile(p, a, e->num_cus);
+          if (tile < 0) fail(FS_ERR_INTERNAL, "no conv tile fits a planned layer");
+          const double kreal = (double)P.kh * P.kw * P.in.C;
+          const double flops = 2.0 * a.M * a.Cout * kreal * g.Z;
+          const double in_b = (double)B * P.in.H * P.in.W * P.in.C * esz * (P.in_slot == SLOT_INPUT ? 1 : g.Z);
+          const double bytes = in_b + ((double)a.Cout * kreal * esz + (double)a.M * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
+          launch(K_CONV, flops, bytes, 1, [&] { launch_conv(a, p, tile, s); });
+          break;
+        }
+        case FS_OP_MAXPOOL:
+        case FS_OP_GAP: {
+          PoolArgs a{};
+          a.x = x; a.x_mstride = x_ms; a.y = y; a.y_mstride = y_ms;
+          a.B = B; a.H = P.in.H; a.W = P.in.W; a.C = P.in.C;
+          a.Ho = P.out.H; a.Wo = P.out.W; a.k = P.kh; a.stride = P.stride; a.pad = P.pad; a.Z = g.Z;
+          const double bytes = ((double)B * P.in.elems() + (double)B * P.out.elems()) * esz * g.Z;
+          if (P.op == FS_OP_MAXPOOL)
+            launch(K_MAXPOOL, 0.0, bytes, 1, [&] { launch_maxpool(a, p, s); });
+          else
+            launch(K_GAP, 0.0, bytes, 1, [&] { launch_gap(a, p, s); });
+          break;
+        }
+        case FS_OP_FC: {
+          FcArgs a{};
+          a.x = x; a.x_mstride = x_ms;
+          a.w = arena + P.w_off; a.w_mstride = P.w_melems;
+          a.bias = reinterpret_cast<const float*>(arena + P.b_off); a.b_mstride = P.b_melems;
+          a.y = y; a.y_mstride = y_ms;
+          a.partial = static_cast<float*>(e->partial.p);
+          a.B = B; a.K = P.K; a.N = P.out.C; a.relu = P.relu; a.out_f32 = P.last ? 1 : 0;
+          a.Z = g.Z;
+          a.split = fc_pick_split(p, B, a.K, a.N, g.Z, e->num_cus);
+          const double flops = 2.0 * B * a.N * (double)a.K * g.Z;
+          const double bytes = ((double)a.N * a.K * esz + (double)B * a.K * esz +
+                                (double)B * a.N * (a.out_f32 ? 4 : esz)) * g.Z;
+          launch(K_FC, flops, bytes, fc_launches(a.split), [&] { launch_fc(a, p, s); });
+          break;
+        }
+      }
+    }
+  }
+
+  SoftmaxArgs sa{};
+  sa.logits = logits;
+  sa.probs = d_probs;
+  sa.mean = d_mean;
+  sa.vote = d_vote;
+  sa.top1 = d_top1;
+  sa.N = e->N;
+  sa.B = B;
+  sa.C = e->C;
+  const double sbytes = (double)e->N * B * e->C * 8 + (d_mean ? (double)B * e->C * 4 : 0) + B * 4.0;
+  launch(K_SOFTMAX, 0.0, sbytes, 1, [&] { launch_softmax_combine(sa, s); });
+  HIPCHK(hipGetLastError());
+}
+
+int launches_per_pass(fs_ensemble* e) {
+  int n = 2;  // preprocess + softmax/combine
+  for (Group& g : e->groups)
+    for (LayerPlan& P : g.layers)
+      n += P.op == FS_OP_FC ? fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus)) : 1;
+  return n;
+}
+
+template <class F>
+fs_status guarded(fs_ensemble* e, F&& fn) {
+  try {
+    fn();
+    if (e) e->err.clear();
+    return FS_OK;
+  } catch (const Error& x) {
+    if (e) e->err = x.msg; else g_thread_error = x.msg;
+    return x.st;
+  } catch (const std::bad_alloc&) {
+    const char* m = "host allocation failed";
+    if (e) e->err = m; else g_thread_error = m;
+    return FS_ERR_OOM;
+  } catch (const std::exception& x) {
+    if (e) e->err = x.what(); else g_thread_error = x.what();
+    return FS_ERR_INTERNAL;
+  } catch (...) {
+    if (e) e->err = "unknown error"; else g_thread_error = "unknown error";
+    return FS_ERR_INTERNAL;
+  }
+}
+
+void destroy_impl(fs_ensemble* e) {
+  if (!e) return;
+  if (hipSetDevice(e->device) == hipSuccess) {
+    if (e->stream) (void)hipStreamSynchronize(e->stream);
+    prof_clear(e);
+    for (hipEvent_t ev : e->ev_pool) (void)hipEventDestroy(ev);
+    e->ev_pool.clear();
+    if (e->stream) (void)hipStreamDestroy(e->stream);
+  }
+  delete e;
+}
+
+// ------------------------------------------------------ test-entry helpers
+struct TmpDev {
+  std::vector<void*> ptrs;
+  void* alloc(size_t n) {
+    void* p = nullptr;
+    HIPCHK(hipMalloc(&p, std::max<size_t>(n, 16)));
+    ptrs.push_back(p);
+    return p;
+  }
+  ~TmpDev() {
+    for (void* p : ptrs) (void)hipFree(p);
+  }
+};
+
+// host fp32 -> device storage type
+void* upload_as(TmpDev& t, const float* src, int64_t n, Prec p) {
+  void* d = t.alloc((size_t)n * es(p));
+  if (p == BF16) {
+    std::vector<uint16_t> h(n);
+    for (int64_t i = 0; i < n; ++i) h[i] = host_bf16(src[i]);
+    HIPCHK(hipMemcpy(d, h.data(), n * 2, hipMemcpyHostToDevice));
+  } else {
+    HIPCHK(hipMemcpy(d, src, n * 4, hipMemcpyHostToDevice));
+  }
+  return d;
+}
+
+void download_as(float* dst, const void* d, int64_t n, Prec p) {
+  if (p == BF16) {
+    std::vector<uint16_t> h(n);
+    HIPCHK(hipMemcpy(h.data(), d, n * 2, hipMemcpyDeviceToHost));
+    for (int64_t i = 0; i < n; ++i) dst[i] = host_bf16_to_f(h[i]);
+  } else {
+    HIPCHK(hipMemcpy(dst, d, n * 4, hipMemcpyDeviceToHost));
+  }
+}
+
+Prec prec_of(int32_t precision) {
+  if (precision != FS_F32 && precision != FS_BF16) fail(FS_ERR_INVALID, "precision must be FS_F32 or FS_BF16");
+  return precision == FS_BF16 ? BF16 : F32;
+}
+
+void check_images(const fs_image* imgs, int B) {
+  if (B < 0) fail(FS_ERR_INVALID, "B must be >= 0");
+  if (B > 0 && !imgs) fail(FS_ERR_INVALID, "images array is NULL");
+  for (int b = 0; b < B; ++b) {
+    const fs_image& im = imgs[b];
+    if (!im.data) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " has no data");
+    if (im.h < 1 || im.w < 1) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " has zero size");
+    if (im.w > (1 << 20) / 3 || im.h > (1 << 20)) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " is too large");
+    if (im.row_stride < 3 * im.w) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " row_stride < 3*w");
+  }
+}
+
+// pack images densely into host memory and descriptors
+size_t packed_size(const fs_image* imgs, int b0, int nb) {
+  size_t n = 0;
+  for (int b = b0; b < b0 + nb; ++b) n += round_up((size_t)imgs[b].h * imgs[b].w * 3, 16);
+  return n;
+}
+void pack_images(const fs_image* imgs, int b0, int nb, uint8_t* dst, ImageDesc* desc) {
+  size_t off = 0;
+  for (int b = b0; b < b0 + nb; ++b) {
+    const fs_image& im = imgs[b];
+    const size_t row = (size_t)im.w * 3;
+    for (int y = 0; y < im.h; ++y) std::memcpy(dst + off + y * row, im.data + (size_t)y * im.row_stride, row);
+    desc[b - b0] = ImageDesc{off, im.h, im.w, (int32_t)row, 0};
+    off += round_up(row * im.h, 16);
+  }
+}
+
+}  // namespace
+
+// ==================================================================== ABI
+extern "C" {
+
+fs_status fs_ensemble_create(const fs_ensemble_desc* desc, fs_ensemble** out) {
+  if (out) *out = nullptr;
+  fs_ensemble* e = nullptr;
+  fs_status st = guarded(nullptr, [&] {
+    if (!out) fail(FS_ERR_INVALID, "out is NULL");
+    validate_desc(desc);
+    e = new fs_ensemble();
+    try {
+      build(e, desc);
+    } catch (...) {
+      destroy_impl(e);
+      e = nullptr;
+      throw;
+    }
+  });
+  if (st == FS_OK) *out = e;
+  return st;
+}
+
+fs_status fs_infer_device(fs_ensemble* e, const uint8_t* d_pixels, const fs_image_desc* d_desc, int32_t B,
+                          float* d_probs, float* d_mean_probs, int32_t* d_vote, int32_t* d_top1,
+                          float* d_logits, void* stream) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    if (B < 1 || B > e->max_batch) fail(FS_ERR_INVALID, "B must be in 1..max_batch for the device path");
+    if (!d_pixels || !d_desc || !d_probs || !d_vote) fail(FS_ERR_INVALID, "required device pointer is NULL");
+    HIPCHK(hipSetDevice(e->device));
+    hipStream_t s = stream ? static_cast<hipStream_t>(stream) : e->stream;
+    run_pass(e, d_pixels, reinterpret_cast<const ImageDesc*>(d_desc), B, d_probs, d_mean_probs, d_vote,
+             d_top1, d_logits, s);
+  });
+}
+
+fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs, float* mean_probs,
+                   int32_t* vote, int32_t* top1, float* logits) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    check_images(imgs, B);
+    if (B == 0) return;
+    if (!probs || !vote) fail(FS_ERR_INVALID, "probs and vote are required");
+    HIPCHK(hipSetDevice(e->device));
+    const int N = e->N, C = e->C, Bm = e->max_batch;
+    hipStream_t s = e->stream;
+    e->d_probs.ensure((size_t)N * Bm * C * 4);
+    e->d_mean.ensure((size_t)Bm * C * 4);
+    e->d_vote.ensure((size_t)Bm * 4);
+    e->d_top1.ensure((size_t)N * Bm * 4);
+    e->d_desc.ensure((size_t)Bm * sizeof(ImageDesc));
+    e->h_desc.ensure((size_t)Bm * sizeof(ImageDesc));
+    const size_t out_floats = (size_t)N * Bm * C * 2 + (size_t)Bm * C;
+    e->h_out.ensure(out_floats * 4 + ((size_t)N + 1) * Bm * 4);
+    for (int b0 = 0; b0 < B; b0 += Bm) {
+      const int nb = std::min(Bm, B - b0);
+      const size_t pbytes = packed_size(imgs, b0, nb);
+      e->h_pixels.ensure(pbytes);
+      e->d_pixels.ensure(pbytes);
+      ImageDesc* hd = static_cast<ImageDesc*>(e->h_desc.p);
+      pack_images(imgs, b0, nb, static_cast<uint8_t*>(e->h_pixels.p), hd);
+      HIPCHK(hipMemcpyAsync(e->d_pixels.p, e->h_pixels.p, pbytes, hipMemcpyHostToDevice, s));
+      HIPCHK(hipMemcpyAsync(e->d_desc.p, hd, nb * sizeof(ImageDesc), hipMemcpyHostToDevice, s));
+      float* dlog = static_cast<float*>(e->logits.p);
+      run_pass(e, static_cast<const uint8_t*>(e->d_pixels.p), static_cast<const ImageDesc*>(e->d_desc.p), nb,
+               static_cast<float*>(e->d_probs.p), mean_probs ? static_cast<float*>(e->d_mean.p) : nullptr,
+               static_cast<int32_t*>(e->d_vote.p), static_cast<int32_t*>(e->d_top1.p), dlog, s);
+      float* hp = static_cast<float*>(e->h_out.p);
+      float* hl = hp + (size_t)N * Bm * C;
+      float* hm = hl + (size_t)N * Bm * C;
+      int32_t* hv = reinterpret_cast<int32_t*>(hm + (size_t)Bm * C);
+      int32_t* ht = hv + Bm;
+      const size_t nbc = (size_t)N * nb * C;
+      HIPCHK(hipMemcpyAsync(hp, e->d_probs.p, nbc * 4, hipMemcpyDeviceToHost, s));
+      if (logits) HIPCHK(hipMemcpyAsync(hl, dlog, nbc * 4, hipMemcpyDeviceToHost, s));
+      if (mean_probs) HIPCHK(hipMemcpyAsync(hm, e->d_mean.p, (size_t)nb * C * 4, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipMemcpyAsync(hv, e->d_vote.p, (size_t)nb * 4, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipMemcpyAsync(ht, e->d_top1.p, (size_t)N * nb * 4, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipStreamSynchronize(s));
+      for (int i = 0; i < N; ++i) {
+        std::memcpy(probs + ((size_t)i * B + b0) * C, hp + (size_t)i * nb * C, (size_t)nb * C * 4);
+        if (logits) std::memcpy(logits + ((size_t)i * B + b0) * C, hl + (size_t)i * nb * C, (size_t)nb * C * 4);
+        if (top1) std::memcpy(top1 + (size_t)i * B + b0, ht + (size_t)i * nb, (size_t)nb * 4);
+      }
+      if (mean_probs) std::memcpy(mean_probs + (size_t)b0 * C, hm, (size_t)nb * C * 4);
+      std::memcpy(vote + b0, hv, (size_t)nb * 4);
+    }
+  });
+}
+
+void fs_destroy(fs_ensemble* e) {
+  try {
+    destroy_impl(e);
+  } catch (...) {
+  }
+}
+
+const char* fs_last_error(const fs_ensemble* e) { return e ? e->err.c_str() : g_thread_error.c_str(); }
+
+fs_status fs_query(const fs_ensemble* ce, fs_info* info) {
+  fs_ensemble* e = const_cast<fs_ensemble*>(ce);
+  if (!e || !info) {
+    g_thread_error = "NULL argument";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    info->num_models = e->N;
+    info->num_classes = e->C;
+    info->max_batch = e->max_batch;
+    info->precision = e->prec == BF16 ? FS_BF16 : FS_F32;
+    info->num_groups = (int32_t)e->groups.size();
+    info->launches_per_pass = launches_per_pass(e);
+    info->weight_bytes = (int64_t)e->arena_bytes;
+    info->workspace_bytes = e->workspace_bytes;
+    info->flops_per_image = e->flops_per_image;
+  });
+}
+
+fs_status fs_profile_enable(fs_ensemble* e, int32_t enable) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    HIPCHK(hipSetDevice(e->device));
+    HIPCHK(hipDeviceSynchronize());
+    prof_clear(e);
+    e->prof_on = enable != 0;
+  });
+}
+
+fs_status fs_profile_read(fs_ensemble* e, fs_kernel_stat* stats, int32_t max_stats, int32_t* n_stats) {
+  if (!e || !stats || !n_stats) {
+    g_thread_error = "NULL argument";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    HIPCHK(hipSetDevice(e->device));
+    fs_kernel_stat acc[K_NCLASS];
+    std::memset(acc, 0, sizeof(acc));
+    for (int c = 0; c < K_NCLASS; ++c) std::snprintf(acc[c].name, sizeof(acc[c].name), "%s", kClassName[c]);
+    for (ProfRec& r : e->prof) {
+      HIPCHK(hipEventSynchronize(r.b));
+      float ms = 0.f;
+      HIPCHK(hipEventElapsedTime(&ms, r.a, r.b));
+      acc[r.cls].launches += r.launches;
+      acc[r.cls].total_ms += ms;
+      acc[r.cls].flops += r.flops;
+      acc[r.cls].bytes += r.bytes;
+    }
+    int n = 0;
+    for (int c = 0; c < K_NCLASS && n < max_stats; ++c)
+      if (acc[c].launches) stats[n++] = acc[c];
+    *n_stats = n;
+  });
+}
+
+// ---------------------------------------------------------- test entries
+fs_status fs_test_preprocess(const fs_image* imgs, int32_t B, int32_t out_h, int32_t out_w, const float mean[3],
+                             const float std_[3], int32_t precision, float* out, int32_t device) {
+  return guarded(nullptr, [&] {
+    Prec p = prec_of(precision);
+    check_images(imgs, B);
+    if (B == 0) return;
+    if (out_h < 1 || out_w < 1 || !mean || !std_ || !out) fail(FS_ERR_INVALID, "bad preprocess arguments");
+    set_device(device);
+    TmpDev t;
+    const size_t pb = packed_size(imgs, 0, B);
+    std::vector<uint8_t> hp(pb);
+    std::vector<ImageDesc> hd(B);
+    pack_images(imgs, 0, B, hp.data(), hd.data());
+    void* dp = t.alloc(pb);
+    void* dd = t.alloc(B * sizeof(ImageDesc));
+    const int64_t n = (int64_t)B * out_h * out_w * 4;
+    void* dout = t.alloc(n * es(p));
+    HIPCHK(hipMemcpy(dp, hp.data(), pb, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(dd, hd.data(), B * sizeof(ImageDesc), hipMemcpyHostToDevice));
+    PreArgs a{};
+    a.pixels = static_cast<const uint8_t*>(dp);
+    a.desc = static_cast<const ImageDesc*>(dd);
+    a.B = B; a.out_h = out_h; a.out_w = out_w;
+    for (int c = 0; c < 3; ++c) { a.mean[c] = mean[c]; a.std_[c] = std_[c]; }
+    a.out = dout;
+    launch_preprocess(a, p, nullptr);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipDeviceSynchronize());
+    download_as(out, dout, n, p);
+  });
+}
+
+fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t Cin, const float* w,
+                       const float* bias, const float* res, int32_t Cout, int32_t kh, int32_t kw, int32_t stride,
+                       int32_t pad, int32_t relu, int32_t precision, int32_t tile, float* out, int32_t device) {
+  return guarded(nullptr, [&] {
+    Prec p = prec_of(precision);
+    if (!in || !w || !out || B < 1 || H < 1 || W < 1 || Cin < 1 || Cout < 1 || kh < 1 || kw < 1 || stride < 1 ||
+        pad < 0)
+      fail(FS_ERR_INVALID, "bad conv arguments");
+    if (H + 2 * pad < kh || W + 2 * pad < kw) fail(FS_ERR_INVALID, "conv output would be empty");
+    if (Cout % 8) fail(FS_ERR_UNSUPPORTED, "Cout must be a multiple of 8");
+    const int cin_p = Cin == 3 ? 4 : Cin;
+    if (Cin != 3 && Cin % (p == BF16 ? 8 : 4)) fail(FS_ERR_UNSUPPORTED, "Cin must be 3 or a multiple of the vector width");
+    const int Ho = (H + 2 * pad - kh) / stride + 1, Wo = (W + 2 * pad - kw) / stride + 1;
+    if ((int64_t)B * H * W * cin_p >= (int64_t(1) << 31) || (int64_t)B * Ho * Wo * Cout >= (int64_t(1) << 31))
+      fail(FS_ERR_UNSUPPORTED, "tensor too large");
+    set_device(device);
+    TmpDev t;
+    std::vector<float> xin;
+    const float* xsrc = in;
+    if (cin_p != Cin) {  // pad the channel dimension with zeros
+      xin.assign((size_t)B * H * W * cin_p, 0.f);
+      for (int64_t px = 0; px < (int64_t)B * H * W; ++px)
+        for (int c = 0; c < Cin; ++c) xin[px * cin_p + c] = in[px * Cin + c];
+      xsrc = xin.data();
+    }
+    void* dx = upload_as(t, xsrc, (int64_t)B * H * W * cin_p, p);
+    fs_layer L{};
+    L.op = FS_OP_CONV; L.cin = Cin; L.cout = Cout; L.kh = kh; L.kw = kw; L.weight = w; L.bias = bias;
+    const int K = kh * kw * cin_p, Kp = (int)round_up(K, CONV_KPAD);
+    std::vector<char> wp((size_t)Cout * Kp * es(p));
+    std::vector<float> bp(Cout);
+    pack_conv(L, cin_p, Kp, p, wp.data(), bp.data());
+    void* dw = t.alloc(wp.size());
+    HIPCHK(hipMemcpy(dw, wp.data(), wp.size(), hipMemcpyHostToDevice));
+    void* db = t.alloc(Cout * 4);
+    HIPCHK(hipMemcpy(db, bp.data(), Cout * 4, hipMemcpyHostToDevice));
+    const int64_t no = (int64_t)B * Ho * Wo * Cout;
+    void* dr = res ? upload_as(t, res, no, p) : nullptr;
+    void* dy = t.alloc(no * es(p));
+    ConvArgs a{};
+    a.x = dx; a.w = dw; a.bias = static_cast<const float*>(db); a.res = dr; a.y = dy;
+    a.B = B; a.H = H; a.W = W; a.Cin = cin_p; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
+    a.kh = kh; a.kw = kw; a.stride = stride; a.pad = pad; a.relu = relu ? 1 : 0;
+    a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = 1;
+    int tl = tile;
+    if (tl < 0) tl = conv_pick_tile(p, a, num_cus_of(device));
+    if (!conv_tile_ok(p, tl, a)) fail(FS_ERR_UNSUPPORTED, "tile " + std::to_string(tile) + " does not fit this conv");
+    launch_conv(a, p, tl, nullptr);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipDeviceSynchronize());
+    download_as(out, dy, no, p);
+  });
+}
+
+fs_status fs_test_maxpool(const float* in, int32_t B, int32_t H, int32_t W, int32_t C, int32_t k, int32_t stride,
+                          int32_t pad, int32_t precision, float* out, int32_t device) {
+  return guarded(nullptr, [&] {
+    Prec p = prec_of(precision);
+    if (!in || !out || B < 1 || H < 1 || W < 1 || C < 1 || k < 1 || stride < 1 || pad < 0 || pad >= k)
+      fail(FS_ERR_INVALID, "bad maxpool arguments");
+    if (C % (p == BF16 ? 8 : 4)) fail(FS_ERR_UNSUPPORTED, "C must be a multiple of the vector width");
+    if (H + 2 * pad < k || W + 2 * pad < k) fail(FS_ERR_INVALID, "pool output would be empty");
+    const int Ho = (H + 2 * pad - k) / stride + 1, Wo = (W + 2 * pad - k) / stride + 1;
+    set_device(device);
+    TmpDev t;
+    void* dx = upload_as(t, in, (int64_t)B * H * W * C, p);
+    const int64_t no = (int64_t)B * Ho * Wo * C;
+    void* dy = t.alloc(no * es(p));
+    PoolArgs a{};
+    a.x = dx; a.y = dy; a.B = B; a.H = H; a.W = W; a.C = C; a.Ho = Ho; a.Wo = Wo;
+    a.k = k; a.stride = stride; a.pad = pad; a.Z = 1;
+    launch_maxpool(a, p, nullptr);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipDeviceSynchronize());
+    download_as(out, dy, no, p);
+  });
+}
+
+fs_status fs_test_gap(const float* in, int32_t B, int32_t H, int32_t W, int32_t C, int32_t precision, float* out,
+                      int32_t device) {
+  return guarded(nullptr, [&] {
+    Prec p = prec_of(precision);
+    if (!in || !out || B < 1 || H < 1 || W < 1 || C < 1) fail(FS_ERR_INVALID, "bad gap arguments");
+    if (C % (p == BF16 ? 8 : 4)) fail(FS_ERR_UNSUPPORTED, "C must be a multiple of the vector width");
+    set_device(device);
+    TmpDev t;
+    void* dx = upload_as(t, in, (int64_t)B * H * W * C, p);
+    void* dy = t.alloc((size_t)B * C * es(p));
+    PoolArgs a{};
+    a.x = dx; a.y = dy; a.B = B; a.H = H; a.W = W; a.C = C; a.Ho = 1; a.Wo = 1; a.Z = 1;
+    launch_gap(a, p, nullptr);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipDeviceSynchronize());
+    download_as(out, dy, (int64_t)B * C, p);
+  });
+}
+
+fs_status fs_test_fc(const float* in, int32_t B, int32_t K, const float* w, const float* bias, int32_t N,
+                     int32_t relu, int32_t precision, int32_t out_storage, float* out, int32_t device) {
+  return guarded(nullptr, [&] {
+    Prec p = prec_of(precision);
+    if (!in || !w || !out || B < 1 || K < 1 || N < 1) fail(FS_ERR_INVALID, "bad fc arguments");
+    if (p == BF16 && K % 8) fail(FS_ERR_UNSUPPORTED, "bf16 K must be a multiple of 8");
+    set_device(device);
+    const int cus = num_cus_of(device);
+    TmpDev t;
+    void* dx = upload_as(t, in, (int64_t)B * K, p);
+    void* dw = upload_as(t, w, (int64_t)N * K, p);
+    std::vector<float> b(N, 0.f);
+    if (bias) std::copy(bias, bias + N, b.begin());
+    void* db = t.alloc(N * 4);
+    HIPCHK(hipMemcpy(db, b.data(), N * 4, hipMemcpyHostToDevice));
+    const bool f32out = !out_storage || p == F32;
+    void* dy = t.alloc((size_t)B * N * (f32out ? 4 : es(p)));
+    FcArgs a{};
+    a.x = dx; a.w = dw; a.bias = static_cast<const float*>(db); a.y = dy;
+    a.B = B; a.K = K; a.N = N; a.relu = relu ? 1 : 0; a.out_f32 = f32out ? 1 : 0; a.Z = 1;
+    a.split = fc_pick_split(p, B, K, N, 1, cus);
+    a.partial = static_cast<float*>(t.alloc(std::max<size_t>(fc_partial_floats(B, N, a.split, 1), 1) * 4));
+    launch_fc(a, p, nullptr);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipDeviceSynchronize());
+    download_as(out, dy, (int64_t)B * N, f32out ? F32 : p);
+  });
+}
+
+fs_status fs_test_softmax_combine(const float* logits, int32_t N, int32_t B, int32_t C, float* probs, float* mean,
+                                  int32_t* vote, int32_t* top1, int32_t device) {
+  return guarded(nullptr, [&] {
+    if (!logits || !probs || !vote || N < 1 || B < 1 || C < 1) fail(FS_ERR_INVALID, "bad softmax arguments");
+    if (C > SOFTMAX_MAX_C) fail(FS_ERR_UNSUPPORTED, "more than 4096 classes");
+    set_device(device);
+    TmpDev t;
+    const size_t n = (size_t)N * B * C;
+    void* dz = t.alloc(n * 4);
+    HIPCHK(hipMemcpy(dz, logits, n * 4, hipMemcpyHostToDevice));
+    void* dp = t.alloc(n * 4);
+    void* dm = t.alloc((size_t)B * C * 4);
+    void* dv = t.alloc((size_t)B * 4);
+    void* dt = t.alloc((size_t)N * B * 4);
+    SoftmaxArgs a{};
+    a.logits = static_cast<const float*>(dz);
+    a.probs = static_cast<float*>(dp);
+    a.mean = mean ? static_cast<float*>(dm) : nullptr;
+    a.vote = static_cast<int32_t*>(dv);
+    a.top1 = top1 ? static_cast<int32_t*>(dt) : nullptr;
+    a.N = N; a.B = B; a.C = C;
+    launch_softmax_combine(a, nullptr);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipDeviceSynchronize());
+    HIPCHK(hipMemcpy(probs, dp, n * 4, hipMemcpyDeviceToHost));
+    if (mean) HIPCHK(hipMemcpy(mean, dm, (size_t)B * C * 4, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(vote, dv, (size_t)B * 4, hipMemcpyDeviceToHost));
+    if (top1) HIPCHK(hipMemcpy(top1, dt, (size_t)N * B * 4, hipMemcpyDeviceToHost));
+  });
+}
+
+int32_t fs_conv_num_tiles(int32_t precision) {
+  if (precision != FS_F32 && precision != FS_BF16) return 0;
+  return conv_num_tiles(precision == FS_BF16 ? BF16 : F32);
+}
+
+const char* fs_conv_tile_name(int32_t precision, int32_t tile) {
+  if (precision != FS_F32 && precision != FS_BF16) return nullptr;
+  const Prec p = precision == FS_BF16 ? BF16 : F32;
+  if (tile < 0 || tile >= conv_num_tiles(p)) return nullptr;
+  return conv_tile(p, tile).name;
+}
+
+}  // extern "C"

@@ -1,0 +1,162 @@
+"""End-to-end parity of the ensemble path (fs_infer / fs_infer_device)
+against the CPU oracle on the seeded workloads, plus invariances.
+
+At the full workload sizes the GPU runs the whole batch exactly as the
+benchmark does, and the oracle computes a sample of the images one by one
+(every image is independent of the others)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from paper_2003_01538_amd import flexserve as fsb
+from tests.parity import compare
+
+pytestmark = pytest.mark.gpu
+MEAN, STD = wl.IMAGENET_MEAN, wl.IMAGENET_STD
+
+
+def _ensemble(w, max_batch=None):
+    return fsb.Ensemble(w["models"], w["out_hw"], MEAN, STD, w["precision"],
+                        max_batch=max_batch or w["batch"])
+
+
+def _images(w):
+    return list(wl.images_uniform(w["image_seed"], w["batch"], *w["in_hw"]))
+
+
+def _check(w, ens, imgs, sample, report=None):
+    g = ens.infer(imgs)
+    o = oracle.ensemble(w["models"], [imgs[i] for i in sample], w["out_hw"], MEAN, STD, w["precision"])
+    compare(g, o, w["precision"], idx=sample, report=report)
+    return g
+
+
+def test_tiny_fp32_b4():
+    w = wl.workload("tiny2_fp32_b4")
+    with _ensemble(w) as ens:
+        g = _check(w, ens, _images(w), list(range(4)))
+        assert np.max(np.abs(g["probs"].astype(np.float64).sum(-1) - 1)) < 1e-5
+        assert np.allclose(g["mean"], g["probs"].mean(0), atol=1e-6)
+
+
+@pytest.mark.parametrize("arch", ["resnet18", "resnet50", "vgg11"])
+def test_fp32_mode_networks_small_inputs(arch):
+    """The strongest indexing check: fp32 storage, so the GPU must agree with
+    the oracle to 1e-4 through every layer of the real architectures."""
+    models = [wl.build_model(arch, 11), wl.build_model(arch, 12)]
+    hw = (64, 64)
+    if arch == "vgg11":  # keep fc1's fan-in: 224 input, one image
+        hw = (224, 224)
+    w = dict(models=models, out_hw=hw, precision="fp32", batch=2)
+    imgs = wl.images_ragged(7, 2, 50, 90)
+    if arch == "vgg11":
+        imgs = imgs[:1]
+    with _ensemble(w, max_batch=2) as ens:
+        g = ens.infer(imgs)
+        o = oracle.ensemble(models, imgs, hw, MEAN, STD, "fp32")
+        compare(g, o, "fp32")
+        assert np.max(np.abs(g["logits"] - o["logits"])) <= 1e-4 * np.abs(o["logits"]).max()
+
+
+def test_resnet18x3_bf16_b32_full_batch_sampled():
+    w = wl.workload("resnet18x3_bf16_b32")
+    imgs = _images(w)
+    with _ensemble(w) as ens:
+        rep = {}
+        _check(w, ens, imgs, [0, 5, 13, 22, 31], report=rep)
+        print("resnet18x3 parity", rep)
+
+
+def test_flexible_batch_stream_requests():
+    s = wl.STREAM_WORKLOAD
+    w = wl.workload(s["ensemble"])
+    reqs = wl.request_stream(s["seed"], 12)
+    with _ensemble(w, max_batch=64) as ens:
+        seen = set()
+        for q in reqs:
+            if len(q) in seen:
+                continue
+            seen.add(len(q))
+            sample = sorted({0, len(q) - 1})
+            _check(w, ens, q, sample)
+        assert len(seen) >= 4
+
+
+def test_hetero_r18_r50_vgg11_b32_sampled():
+    w = wl.workload("hetero_r18_r50_vgg11_bf16_b32")
+    with _ensemble(w) as ens:
+        assert ens.info()["num_groups"] == 3
+        rep = {}
+        _check(w, ens, _images(w), [0, 31], report=rep)
+        print("hetero parity", rep)
+
+
+def test_resnet50x5_b256_sampled():
+    w = wl.workload("resnet50x5_bf16_b256")
+    with _ensemble(w) as ens:
+        assert ens.info()["num_groups"] == 1
+        rep = {}
+        _check(w, ens, _images(w), [0, 255], report=rep)
+        print("resnet50x5 parity", rep)
+
+
+def test_determinism_permutation_and_device_path():
+    import torch
+    w = wl.workload("resnet18x3_bf16_b32")
+    imgs = _images(w)[:16]
+    with _ensemble(w, max_batch=32) as ens:
+        g0 = ens.infer(imgs)
+        for _ in range(3):
+            g1 = ens.infer(imgs)
+            for k in ("probs", "logits", "vote", "top1", "mean"):
+                assert np.array_equal(g0[k], g1[k]), k
+        perm = np.random.default_rng(0).permutation(16)
+        gp = ens.infer([imgs[i] for i in perm])
+        assert np.array_equal(gp["logits"], g0["logits"][:, perm])
+        assert np.array_equal(gp["vote"], g0["vote"][perm])
+        # device-resident entry point on torch-owned memory gives the same bits
+        flat, desc = wl.pack_images(imgs)
+        d_pix = torch.from_numpy(flat).cuda()
+        d_desc = torch.tensor([[o, h | (w_ << 32), rs] for o, h, w_, rs in desc], dtype=torch.int64).cuda()
+        N, B, C = 3, 16, 1000
+        d_probs = torch.empty((N, B, C), dtype=torch.float32, device="cuda")
+        d_logits = torch.empty_like(d_probs)
+        d_mean = torch.empty((B, C), dtype=torch.float32, device="cuda")
+        d_vote = torch.empty(B, dtype=torch.int32, device="cuda")
+        d_top1 = torch.empty((N, B), dtype=torch.int32, device="cuda")
+        stream = torch.cuda.current_stream()
+        fsb.fs_infer_device(ens.handle, d_pix.data_ptr(), d_desc.data_ptr(), B, d_probs.data_ptr(),
+                            d_mean.data_ptr(), d_vote.data_ptr(), d_top1.data_ptr(),
+                            d_logits.data_ptr(), stream.cuda_stream)
+        torch.cuda.synchronize()
+        assert np.array_equal(d_logits.cpu().numpy(), g0["logits"])
+        assert np.array_equal(d_probs.cpu().numpy(), g0["probs"])
+        assert np.array_equal(d_vote.cpu().numpy(), g0["vote"])
+        with pytest.raises(fsb.FsError):
+            fsb.fs_infer_device(ens.handle, d_pix.data_ptr(), d_desc.data_ptr(), 33, d_probs.data_ptr(),
+                                0, d_vote.data_ptr(), 0, 0, stream.cuda_stream)
+
+
+def test_chunked_batches_and_empty_batch():
+    w = wl.workload("tiny2_fp32_b4")
+    imgs = wl.images_ragged(5, 11, 20, 48)
+    with _ensemble(dict(w, batch=4), max_batch=4) as ens:
+        g = ens.infer(imgs)  # 4 + 4 + 3
+        o = oracle.ensemble(w["models"], imgs, w["out_hw"], MEAN, STD, "fp32")
+        compare(g, o, "fp32")
+        e = ens.infer([])
+        assert e["probs"].shape == (2, 0, 10)
+
+
+def test_profiler_counts_every_launch():
+    w = wl.workload("resnet18x3_bf16_b32")
+    with _ensemble(w) as ens:
+        info = ens.info()
+        fsb.fs_profile_enable(ens.handle, True)
+        ens.infer(_images(w))
+        st = fsb.fs_profile_read(ens.handle)
+        fsb.fs_profile_enable(ens.handle, False)
+        assert sum(v["launches"] for v in st.values()) == info["launches_per_pass"]
+        assert st["conv"]["launches"] == 20 and st["conv"]["total_ms"] > 0
+        assert abs(st["conv"]["flops"] / 32 - info["flops_per_image"]) / info["flops_per_image"] < 0.01

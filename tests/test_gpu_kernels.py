@@ -1,0 +1,212 @@
+"""Per-kernel parity of the HIP path against the CPU oracle, element by
+element, on the same seeded inputs (the single-kernel C entry points).
+
+Tolerances (derived from the arithmetic):
+* fp32 storage: |gpu - oracle| <= 1e-5 * sum|x*w| + 1e-6 (an fp32 sum in
+  another order against a double sum).
+* bf16 storage: |gpu - oracle| <= 1 bf16 ulp of the oracle value +
+  2^-16 * sum|x*w|, and at least 99% of the outputs bit-identical.
+* max pool: bit-exact.  Softmax: 1e-6 absolute."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from paper_2003_01538_amd import flexserve as fsb
+
+pytestmark = pytest.mark.gpu
+MEAN, STD = wl.IMAGENET_MEAN, wl.IMAGENET_STD
+F32, BF16 = fsb.FS_F32, fsb.FS_BF16
+PREC = {F32: "fp32", BF16: "bf16"}
+
+
+def ulp_bf16(x):
+    x = np.abs(np.asarray(x, np.float32))
+    e = np.floor(np.log2(np.maximum(x, np.float32(2.0 ** -126))))
+    return np.float32(2.0) ** (e - 7)
+
+
+def assert_bf16_close(g, o, absacc=None, frac_exact=0.99, what=""):
+    g, o = np.asarray(g, np.float32), np.asarray(o, np.float32)
+    tol = ulp_bf16(o) + (0 if absacc is None else 2.0 ** -16 * absacc)
+    bad = np.abs(g - o) > tol
+    assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} outside 1 ulp + bound; max err {np.abs(g - o).max()}"
+    exact = np.mean(g.view(np.uint32) == o.view(np.uint32))
+    assert exact >= frac_exact, f"{what}: only {exact:.4f} bit-identical"
+
+
+# ----------------------------------------------------------------- preprocess
+@pytest.mark.parametrize("prec", [F32, BF16])
+@pytest.mark.parametrize("case", ["identity32", "resize256to224", "ragged", "tiny_up"])
+def test_preprocess_parity(gpu_lib, prec, case):
+    rng = np.random.default_rng(sum(map(ord, case)))
+    if case == "identity32":
+        imgs, oh, ow = list(wl.images_uniform(1000, 4, 32, 32)), 32, 32
+    elif case == "resize256to224":
+        imgs, oh, ow = list(wl.images_uniform(2000, 3, 256, 256)), 224, 224
+    elif case == "ragged":
+        imgs, oh, ow = wl.images_ragged(3000, 5), 224, 224
+    else:
+        imgs = [rng.integers(0, 256, (1, 1, 3), dtype=np.uint8),
+                rng.integers(0, 256, (3, 7, 3), dtype=np.uint8)]
+        oh, ow = 17, 9
+    # a strided view: rows longer than 3*w bytes
+    big = rng.integers(0, 256, (40, 50, 3), dtype=np.uint8)
+    imgs = list(imgs) + [big[5:37, 3:41]]
+    g = fsb.fs_test_preprocess(imgs, oh, ow, MEAN, STD, prec)
+    assert np.all(g[..., 3] == 0)
+    for i, im in enumerate(imgs):
+        o = oracle.preprocess(im, oh, ow, MEAN, STD, PREC[prec])
+        if prec == F32:
+            assert np.max(np.abs(g[i, ..., :3] - o)) <= 1e-5, (case, i)
+        else:
+            assert_bf16_close(g[i, ..., :3], o, frac_exact=0.99, what=f"{case}[{i}]")
+
+
+# ----------------------------------------------------------------------- conv
+CONV_CASES = [
+    # B, H, W, Cin, Cout, k, stride, pad, relu, residual
+    (2, 32, 32, 3, 64, 7, 2, 3, 1, 0),     # ResNet stem shape (Cin padded to 4)
+    (2, 20, 20, 3, 64, 3, 1, 1, 1, 0),     # VGG first conv shape
+    (2, 14, 14, 64, 64, 3, 1, 1, 1, 1),    # basic block conv + residual + ReLU
+    (3, 15, 13, 64, 128, 3, 2, 1, 1, 0),   # strided, ragged M
+    (2, 14, 14, 64, 128, 1, 2, 0, 0, 0),   # 1x1 downsample
+    (1, 7, 7, 256, 512, 3, 1, 1, 0, 1),    # deep layer, residual, no ReLU
+    (2, 9, 9, 128, 256, 1, 1, 0, 1, 1),    # bottleneck expand + residual
+    (1, 5, 6, 16, 32, 3, 1, 1, 1, 0),      # tiny-net second conv
+]
+
+
+def _conv_inputs(case, prec, seed):
+    B, H, W, Cin, Cout, k, s, p, relu, has_res = case
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((B, H, W, Cin)).astype(np.float32)
+    w = (rng.standard_normal((Cout, k, k, Cin)) * np.sqrt(2.0 / (Cin * k * k))).astype(np.float32)
+    b = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
+    Ho, Wo = (H + 2 * p - k) // s + 1, (W + 2 * p - k) // s + 1
+    r = rng.standard_normal((B, Ho, Wo, Cout)).astype(np.float32) if has_res else None
+    if prec == BF16:
+        x, w = oracle.round_bf16(x), oracle.round_bf16(w)
+        r = None if r is None else oracle.round_bf16(r)
+    return x, w, b, r
+
+
+def _tiles_for(prec, Cin):
+    out = []
+    for t in range(fsb.fs_conv_num_tiles(prec)):
+        name = fsb.fs_conv_tile_name(prec, t)
+        vec = int(name.rsplit("_v", 1)[1])
+        cin_p = 4 if Cin == 3 else Cin
+        if cin_p % vec == 0:
+            out.append(t)
+    return out
+
+
+@pytest.mark.parametrize("prec", [BF16, F32])
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)))
+def test_conv_parity_every_tile(gpu_lib, prec, ci):
+    case = CONV_CASES[ci]
+    B, H, W, Cin, Cout, k, s, p, relu, has_res = case
+    x, w, b, r = _conv_inputs(case, prec, 100 + ci)
+    o, ab = oracle.conv2d(x, w, b, s, p, relu, r, PREC[prec], want_abs=True)
+    tiles = _tiles_for(prec, Cin)
+    assert tiles
+    for t in tiles + [-1]:
+        g = fsb.fs_test_conv(x, w, b, r, s, p, relu, prec, tile=t)
+        if prec == BF16:
+            assert_bf16_close(g, o, ab, what=f"case {ci} tile {t}")
+        else:
+            assert np.all(np.abs(g - o) <= 1e-5 * ab + 1e-6), f"case {ci} tile {t}: {np.abs(g - o).max()}"
+
+
+def test_conv_repeat_is_bit_identical(gpu_lib):
+    x, w, b, r = _conv_inputs(CONV_CASES[2], BF16, 7)
+    g0 = fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16)
+    for _ in range(5):
+        assert np.array_equal(fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16), g0)
+
+
+# -------------------------------------------------------------------- pooling
+@pytest.mark.parametrize("prec", [BF16, F32])
+@pytest.mark.parametrize("k,s,p,hw", [(3, 2, 1, (17, 16)), (2, 2, 0, (16, 14)), (3, 2, 1, (112, 112))])
+def test_maxpool_bit_exact(gpu_lib, prec, k, s, p, hw):
+    rng = np.random.default_rng(k * 10 + hw[0])
+    x = rng.standard_normal((2,) + hw + (64,)).astype(np.float32)
+    if prec == BF16:
+        x = oracle.round_bf16(x)
+    g = fsb.fs_test_maxpool(x, k, s, p, prec)
+    assert np.array_equal(g, oracle.maxpool(x, k, s, p))
+
+
+@pytest.mark.parametrize("prec", [BF16, F32])
+@pytest.mark.parametrize("shape", [(3, 7, 7, 512), (2, 7, 7, 2048), (4, 16, 16, 32)])
+def test_gap_parity(gpu_lib, prec, shape):
+    rng = np.random.default_rng(shape[-1])
+    x = np.abs(rng.standard_normal(shape)).astype(np.float32)
+    if prec == BF16:
+        x = oracle.round_bf16(x)
+    g = fsb.fs_test_gap(x, prec)
+    o = oracle.gap(x, PREC[prec])
+    if prec == BF16:
+        assert_bf16_close(g, o, frac_exact=0.99, what="gap")
+    else:
+        assert np.max(np.abs(g - o)) <= 1e-6 * np.abs(o).max()
+
+
+# ------------------------------------------------------------------------- fc
+@pytest.mark.parametrize("prec", [BF16, F32])
+@pytest.mark.parametrize("B,K,N,relu,out_storage", [
+    (32, 512, 1000, 0, 0),     # ResNet-18 head
+    (5, 2048, 1000, 0, 0),     # ResNet-50 head, ragged batch
+    (3, 25088, 64, 1, 1),      # VGG fc1 fan-in (split-K), hidden output
+    (70, 4096, 96, 1, 1),      # more than 64 images
+    (4, 32, 10, 0, 0),         # tiny head
+    (1, 512, 1000, 0, 0),
+])
+def test_fc_parity(gpu_lib, prec, B, K, N, relu, out_storage):
+    rng = np.random.default_rng(B * 7 + K)
+    x = rng.standard_normal((B, K)).astype(np.float32)
+    w = (rng.standard_normal((N, K)) * np.sqrt(2.0 / K)).astype(np.float32)
+    b = (rng.standard_normal(N) * 0.1).astype(np.float32)
+    if prec == BF16:
+        x, w = oracle.round_bf16(x), oracle.round_bf16(w)
+    st = "bf16" if (prec == BF16 and out_storage) else "fp32"
+    o = oracle.fc(x, w, b, relu, st)
+    ab = np.abs(x).astype(np.float64) @ np.abs(w).astype(np.float64).T
+    g = fsb.fs_test_fc(x, w, b, relu, prec, out_storage)
+    if st == "bf16":
+        assert_bf16_close(g, o, ab, what="fc")
+    else:
+        assert np.all(np.abs(g - o) <= 1e-5 * ab + 1e-6), np.abs(g - o).max()
+
+
+# -------------------------------------------------------- softmax + combine
+@pytest.mark.parametrize("N,B,C,scale", [(3, 32, 1000, 80.0), (5, 7, 1000, 3.0), (2, 4, 10, 2.0),
+                                         (1, 3, 4096, 1.0), (4, 2, 257, 0.0)])
+def test_softmax_combine_parity(gpu_lib, N, B, C, scale):
+    rng = np.random.default_rng(N * 100 + C)
+    z = (rng.standard_normal((N, B, C)) * scale).astype(np.float32)
+    g = fsb.fs_test_softmax_combine(z)
+    p = oracle.softmax(z)
+    o = oracle.combine(p, z)
+    assert np.max(np.abs(g["probs"] - p)) <= 1e-6
+    assert np.max(np.abs(g["mean"] - o["mean"])) <= 1e-6
+    assert np.array_equal(g["top1"], o["top1"])  # logits are exact inputs: same argmax
+    S = o["S"]
+    for b in range(B):
+        top2 = np.sort(S[b])[-2:] if C > 1 else S[b]
+        if C == 1 or top2[1] - top2[0] > 2 * N * 1e-6:
+            assert g["vote"][b] == o["vote"][b]
+        else:
+            assert S[b, g["vote"][b]] >= S[b].max() - 2 * N * 1e-6
+
+
+def test_softmax_combine_exact_ties_take_lowest_index(gpu_lib):
+    z = np.full((2, 3, 50), -1e4, np.float32)
+    z[0, :, 31] = 0.0   # model 0 saturates on 31
+    z[1, :, 12] = 0.0   # model 1 saturates on 12: S ties at 1.0
+    z[0, 1, 5] = 0.0    # model 0, image 1: exact logit tie 5 vs 31
+    g = fsb.fs_test_softmax_combine(z)
+    # image 1: model 0 splits 0.5/0.5 over 5 and 31, so S[12] = 1 still wins
+    assert g["vote"].tolist() == [12, 12, 12]
+    assert g["top1"][0].tolist() == [31, 5, 31] and g["top1"][1].tolist() == [12, 12, 12]
