@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--workload", default="resnet18x3_bf16_b32")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="bound on the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--dump-launches", default="",
+                    help="write the per-launch event times of one profiled step to this JSON file")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
@@ -121,6 +123,11 @@ def main():
         torch.cuda.synchronize()
         prof_s = time.perf_counter() - t0
         stats = fsb.fs_profile_read(ens.handle)
+        if args.dump_launches:
+            per_step = info["launches_per_pass"]
+            recs = fsb.fs_profile_launches(ens.handle, max_out=per_step * args.steps)
+            with open(args.dump_launches, "w") as f:
+                json.dump(recs[-per_step:], f, indent=0)
         fsb.fs_profile_enable(ens.handle, False)
         cv = stats["conv"]
         per_launch_ms = cv["total_ms"] / cv["launches"]

@@ -88,13 +88,17 @@ typedef struct {
     int32_t device;     /* HIP device ordinal */
 } fs_ensemble_desc;
 
-/* A host image: uint8 HWC RGB, h rows of row_stride bytes (>= 3*w). */
+/* A host image: uint8 HWC RGB, h rows of row_stride bytes (>= 3*w),
+ * 1 <= h, w <= 32768. */
 typedef struct {
     const uint8_t *data;
     int32_t h, w, row_stride;
 } fs_image;
 
-/* A device-resident image: offset (bytes) into a packed uint8 buffer. */
+/* A device-resident image: offset (bytes) into a packed uint8 buffer; the
+ * caller guarantees 1 <= h, w <= 32768, row_stride >= 3*w and that all
+ * h*row_stride bytes lie inside the buffer (the device path reads them
+ * without a host-side check). */
 typedef struct {
     uint64_t offset;
     int32_t h, w, row_stride, reserved;
@@ -160,6 +164,21 @@ fs_status fs_profile_enable(fs_ensemble *e, int32_t enable); /* (re)starts, clea
 fs_status fs_profile_read(fs_ensemble *e, fs_kernel_stat *stats, int32_t max_stats,
                           int32_t *n_stats);
 
+/* The individual launches recorded since fs_profile_enable, in order (up to
+ * max_out): kernel class and variant, group/layer of the plan (-1 outside
+ * the layer list), GEMM shape M x N x K of conv/fc, models per launch Z, event
+ * time and algorithmic FLOP/bytes.  Synchronises like fs_profile_read. */
+typedef struct {
+    char kclass[16];
+    char kernel[32];
+    int32_t group, layer, M, N, K, Z;
+    double ms;
+    double flops;
+    double bytes;
+} fs_launch_stat;
+fs_status fs_profile_launches(fs_ensemble *e, fs_launch_stat *out, int32_t max_out,
+                              int32_t *n_out);
+
 /* ---- single-kernel entry points on host tensors (synchronous; for parity
  * tests).  precision selects fp32 or bf16 storage; in bf16 the inputs must
  * already be bf16-representable and outputs are returned widened to fp32. */
@@ -197,6 +216,16 @@ fs_status fs_test_fc(const float *in, int32_t B, int32_t K, const float *w, cons
 fs_status fs_test_softmax_combine(const float *logits, int32_t N, int32_t B, int32_t C,
                                   float *probs, float *mean, int32_t *vote, int32_t *top1,
                                   int32_t device);
+
+/* Measurement of one convolution layer shape: Z models' weights, one
+ * shared input filled with a constant, `iters` back-to-back launches of tile
+ * configuration `tile` (-1 = the planner's choice, reported in *tile_used),
+ * timed with HIP events; *avg_ms is the mean time of one launch.  Used to
+ * choose and evidence tile configurations per batch size. */
+fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Cout, int32_t kh,
+                        int32_t kw, int32_t stride, int32_t pad, int32_t relu, int32_t residual,
+                        int32_t precision, int32_t tile, int32_t Z, int32_t iters, double *avg_ms,
+                        int32_t *tile_used, int32_t device);
 
 /* Number of conv tile configurations fs_test_conv accepts (0..n-1) for a
  * precision, and the name of tile t (NULL when out of range). */

@@ -5,8 +5,9 @@
 // n = output channel, reduction k = (ky, kx, ci) with ci fastest.  The
 // A tile (BM x BK) is gathered on the fly from the input (zero outside the
 // image), the B tile (BN x BK) is a slice of the packed weights
-// [Cout][Kp].  Both are staged through LDS with two buffers: the global
-// loads of tile k+1 are in flight while the MFMAs consume tile k.  The
+// [Cout][Kp].  Both are staged through two LDS buffers fed from two
+// register sets: the global loads of tile k+2 are in flight while the MFMAs
+// consume tile k from LDS and tile k+1 waits in registers.  The
 // fp32 accumulators are written to LDS after the reduction and read back
 // row-contiguous, so bias, residual, ReLU and the rounding store are done
 // with 16-byte coalesced accesses.
@@ -38,8 +39,24 @@ template <> struct VecT<8> { using T = uint2; };
 constexpr int NT = 256;          // threads per workgroup (4 waves)
 constexpr int ROWB = 128 + 16;   // LDS bytes per tile row: 128 B of data + 16 B pad
 
-template <int P, int BM, int BN, int VEC>
-__global__ void __launch_bounds__(NT, 2) k_conv(ConvArgs a) {
+constexpr uint32_t OOB = 0x80000000u;  // buffer offset past every tensor: loads return 0
+constexpr int RSRC_DW3 = 0x00020000;    // raw (untyped) buffer resource, gfx9 family
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, RSRC_DW3);
+}
+template <int BYTES>
+__device__ __forceinline__ typename VecT<BYTES>::T buf_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  if constexpr (BYTES == 16)
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  else
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+
+// FAST: Cin is a multiple of BK, so every K-tile lies inside one filter tap
+// (ky, kx) and a contiguous channel range: the tap is wave-uniform.
+template <int P, int BM, int BN, int VEC, bool FAST>
+__global__ void __launch_bounds__(NT, BM >= 256 ? 1 : 2) k_conv(ConvArgs a) {
   using T = typename PT<P>::T;
   constexpr int BK = PT<P>::BK, KSTEP = PT<P>::KSTEP;
   constexpr int ES = sizeof(T);
@@ -69,12 +86,16 @@ __global__ void __launch_bounds__(NT, 2) k_conv(ConvArgs a) {
   const int mt = tile / tiles_n, ntile = tile - mt * tiles_n;
   const int m0 = mt * BM, n0 = ntile * BN;
 
-  const T* __restrict__ x = reinterpret_cast<const T*>(a.x) + z * a.x_mstride;
-  const T* __restrict__ w = reinterpret_cast<const T*>(a.w) + z * a.w_mstride;
+  // Buffer resources: out-of-range offsets (padding taps, rows past M,
+  // columns past Cout) read as zero without a branch.
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(reinterpret_cast<const T*>(a.x) + z * a.x_mstride,
+                                              (uint32_t)((int64_t)a.B * a.H * a.W * a.Cin * ES));
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(reinterpret_cast<const T*>(a.w) + z * a.w_mstride,
+                                              (uint32_t)((int64_t)a.Cout * a.Kp * ES));
 
   // ---- per-thread A rows: fixed for the whole reduction
   const int aj = tid % AKV;           // which vector of the row
-  int a_off[AP], a_iy[AP], a_ix[AP];  // image base offset, top-left input tap
+  int a_off[AP], a_iy[AP], a_ix[AP];  // offset of (b, iy0, ix0) + this thread's channels; top-left tap
   const int HoWo = a.Ho * a.Wo;
 #pragma unroll
   for (int p = 0; p < AP; ++p) {
@@ -82,9 +103,9 @@ __global__ void __launch_bounds__(NT, 2) k_conv(ConvArgs a) {
     if (m < a.M) {
       int b = m / HoWo, r = m - b * HoWo;
       int oy = r / a.Wo, ox = r - oy * a.Wo;
-      a_off[p] = b * a.H * a.W * a.Cin;
       a_iy[p] = oy * a.stride - a.pad;
       a_ix[p] = ox * a.stride - a.pad;
+      a_off[p] = ((b * a.H + a_iy[p]) * a.W + a_ix[p]) * a.Cin + aj * VEC;
     } else {
       a_off[p] = 0;
       a_iy[p] = -(1 << 28);  // never inside the image
@@ -102,44 +123,50 @@ __global__ void __launch_bounds__(NT, 2) k_conv(ConvArgs a) {
   }
   // ---- B rows
   const int bj = tid % BKV;
-  const T* b_ptr[BP];
-  bool b_ok[BP];
+  uint32_t b_off[BP];  // byte offset of this thread's weight vector, OOB past Cout
 #pragma unroll
   for (int p = 0; p < BP; ++p) {
     int n = n0 + p * BRPP + tid / BKV;
-    b_ok[p] = (n < a.Cout) && (p * BRPP + tid / BKV < BN);
-    b_ptr[p] = w + (int64_t)(b_ok[p] ? n : 0) * a.Kp + bj * BVE;
+    b_off[p] = (n < a.Cout) ? (uint32_t)((n * a.Kp + bj * BVE) * ES) : OOB;
   }
 
-  AV ra[AP];
-  uint4 rb[BP];
-  auto load_tiles = [&](int kt) {
-    const bool kvalid = ky < a.kh;
+  // Two register staging sets: the global loads of tile k+2 are in flight
+  // while tile k is consumed from LDS and tile k+1 waits in registers.
+  AV ra0[AP], ra1[AP];
+  uint4 rb0[BP], rb1[BP];
+  auto load_tiles = [&](AV* ra, uint4* rb, int kt) {
+    int tky, tkx, tci;
+    if constexpr (FAST) {  // wave-uniform tap of this K-tile
+      const int k0 = kt * BK;
+      const int tap = k0 / a.Cin;
+      tci = k0 - tap * a.Cin;
+      tky = tap / a.kw;
+      tkx = tap - tky * a.kw;
+    } else {
+      tky = ky; tkx = kx; tci = ci - aj * VEC;
+    }
+    const bool kvalid = tky < a.kh;
+    const int tap_off = (tky * a.W + tkx) * a.Cin + tci;
 #pragma unroll
     for (int p = 0; p < AP; ++p) {
-      int iy = a_iy[p] + ky, ix = a_ix[p] + kx;
-      bool ok = kvalid && (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-      if (ok)
-        ra[p] = *reinterpret_cast<const AV*>(x + a_off[p] + (iy * a.W + ix) * a.Cin + ci);
-      else
-        ra[p] = AV{};
+      const int iy = a_iy[p] + tky, ix = a_ix[p] + tkx;
+      const bool ok = kvalid && (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+      ra[p] = buf_load<AVB>(rx, ok ? (uint32_t)((a_off[p] + tap_off) * ES) : OOB);
     }
 #pragma unroll
-    for (int p = 0; p < BP; ++p) {
-      if (b_ok[p])
-        rb[p] = *reinterpret_cast<const uint4*>(b_ptr[p] + kt * BK);
-      else
-        rb[p] = uint4{0, 0, 0, 0};
-    }
+    for (int p = 0; p < BP; ++p)
+      rb[p] = buf_load<16>(rw, b_off[p] == OOB ? OOB : b_off[p] + (uint32_t)(kt * BK * ES));
   };
   auto advance_k = [&]() {
-    ci += BK;
-    while (ci >= a.Cin) {
-      ci -= a.Cin;
-      if (++kx == a.kw) { kx = 0; ++ky; }
+    if constexpr (!FAST) {
+      ci += BK;
+      while (ci >= a.Cin) {
+        ci -= a.Cin;
+        if (++kx == a.kw) { kx = 0; ++ky; }
+      }
     }
   };
-  auto store_tiles = [&](int buf) {
+  auto store_tiles = [&](int buf, const AV* ra, const uint4* rb) {
     char* As = smem + buf * STAGE;
     char* Bs = As + BM * ROWB;
 #pragma unroll
@@ -192,21 +219,30 @@ __global__ void __launch_bounds__(NT, 2) k_conv(ConvArgs a) {
     }
   };
 
-  // ---- main loop, two LDS buffers
+  // ---- main loop: two LDS buffers, two register sets (prefetch distance 2)
   const int nk = a.Kp / BK;
-  load_tiles(0);
-  store_tiles(0);
+  load_tiles(ra0, rb0, 0);
+  advance_k();
+  if (nk > 1) {
+    load_tiles(ra1, rb1, 1);
+    advance_k();
+  }
+  store_tiles(0, ra0, rb0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
+  // iteration kt: LDS[kt & 1] holds tile kt, registers set (kt+1) & 1 hold
+  // tile kt+1, and set kt & 1 is free for tile kt+2.
+  auto iter = [&](int kt, AV* ra_free, uint4* rb_free, const AV* ra_next, const uint4* rb_next) {
+    if (kt + 2 < nk) {
+      load_tiles(ra_free, rb_free, kt + 2);
       advance_k();
-      load_tiles(kt + 1);
     }
-    compute(cur);
-    if (more) store_tiles(cur ^ 1);
+    compute(kt & 1);
+    if (kt + 1 < nk) store_tiles((kt + 1) & 1, ra_next, rb_next);
     __syncthreads();
+  };
+  for (int kt = 0; kt < nk; kt += 2) {
+    iter(kt, ra0, rb0, ra1, rb1);
+    if (kt + 1 < nk) iter(kt + 1, ra1, rb1, ra0, rb0);
   }
 
   // ---- epilogue: accumulators -> LDS -> coalesced rows
@@ -267,6 +303,7 @@ static const ConvTile kTilesBF16[] = {
     {64, 64, 8, "bf16_64x64_v8"},
     {128, 64, 4, "bf16_128x64_v4"},
     {64, 64, 4, "bf16_64x64_v4"},
+    {256, 64, 8, "bf16_256x64_v8"},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -308,7 +345,10 @@ int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus) {
 template <int P, int BM, int BN, int VEC>
 static void launch_t(const ConvArgs& a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.Cout + BN - 1) / BN) * a.Z;
-  hipLaunchKernelGGL((k_conv<P, BM, BN, VEC>), dim3(tiles), dim3(NT), 0, s, a);
+  if (a.Cin % PT<P>::BK == 0)
+    hipLaunchKernelGGL((k_conv<P, BM, BN, VEC, true>), dim3(tiles), dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_conv<P, BM, BN, VEC, false>), dim3(tiles), dim3(NT), 0, s, a);
 }
 
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
@@ -319,6 +359,7 @@ void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
       case 2: launch_t<BF16, 64, 64, 8>(a, s); break;
       case 3: launch_t<BF16, 128, 64, 4>(a, s); break;
       case 4: launch_t<BF16, 64, 64, 4>(a, s); break;
+      case 5: launch_t<BF16, 256, 64, 8>(a, s); break;
       default: break;
     }
   } else {

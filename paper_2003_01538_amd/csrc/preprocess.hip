@@ -25,14 +25,19 @@ __global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
   const ImageDesc d = a.desc[b];
   const uint8_t* img = a.pixels + d.offset;
 
-  const float sh = (float)d.h / (float)a.out_h;
-  const float sw = (float)d.w / (float)a.out_w;
-  float sy = fmaxf(((float)oy + 0.5f) * sh - 0.5f, 0.0f);
-  float sx = fmaxf(((float)ox + 0.5f) * sw - 0.5f, 0.0f);
-  int y0 = min((int)sy, d.h - 1), x0 = min((int)sx, d.w - 1);
-  int y1 = min(y0 + 1, d.h - 1), x1 = min(x0 + 1, d.w - 1);
-  float ly = sy - (float)y0, lx = sx - (float)x0;
-  float hy = 1.0f - ly, hx = 1.0f - lx;
+  // Source coordinate s = ((2o + 1) * in - out) / (2 * out), clamped at 0:
+  // the integer part and the fraction come from exact integer arithmetic,
+  // so only the fraction itself is rounded (relative error 2^-24).
+  const int ny = (2 * oy + 1) * d.h - a.out_h, dy = 2 * a.out_h;
+  const int nx = (2 * ox + 1) * d.w - a.out_w, dx = 2 * a.out_w;
+  int y0 = 0, x0 = 0;
+  float ly = 0.f, lx = 0.f;
+  if (ny > 0) { y0 = ny / dy; ly = (float)(ny - y0 * dy) / (float)dy; }
+  if (nx > 0) { x0 = nx / dx; lx = (float)(nx - x0 * dx) / (float)dx; }
+  y0 = min(y0, d.h - 1);
+  x0 = min(x0, d.w - 1);
+  const int y1 = min(y0 + 1, d.h - 1), x1 = min(x0 + 1, d.w - 1);
+  const float hy = 1.0f - ly, hx = 1.0f - lx;
 
   const uint8_t* r0 = img + (int64_t)y0 * d.row_stride;
   const uint8_t* r1 = img + (int64_t)y1 * d.row_stride;

@@ -131,6 +131,8 @@ struct ProfRec {
   hipEvent_t a, b;
   double flops, bytes;
   int launches;
+  int group, layer, M, N, K, Z;
+  const char* kernel;
 };
 
 }  // namespace
@@ -242,13 +244,13 @@ void validate_desc(const fs_ensemble_desc* d) {
         default:
           fail(FS_ERR_INVALID, lp + "unknown op");
       }
-      if (out[i].elems() * (int64_t)d->max_batch >= (int64_t(1) << 31))
-        fail(FS_ERR_UNSUPPORTED, lp + "activation tensor too large for max_batch (2^31 elements)");
+      if (out[i].elems() * (int64_t)d->max_batch * (prec == FS_BF16 ? 2 : 4) >= (int64_t(1) << 31))
+        fail(FS_ERR_UNSUPPORTED, lp + "activation tensor of max_batch images exceeds 2 GiB");
     }
     if (s.layers[s.num_layers - 1].op != FS_OP_FC) fail(FS_ERR_INVALID, pfx + "the last layer must be fc");
   }
-  if ((int64_t)d->pre.out_h * d->pre.out_w * 4 * d->max_batch >= (int64_t(1) << 31))
-    fail(FS_ERR_UNSUPPORTED, "transformed input too large for max_batch");
+  if ((int64_t)d->pre.out_h * d->pre.out_w * 4 * d->max_batch * (prec == FS_BF16 ? 2 : 4) >= (int64_t(1) << 31))
+    fail(FS_ERR_UNSUPPORTED, "transformed input of max_batch images exceeds 2 GiB");
 }
 
 bool same_structure(const fs_model_spec& a, const fs_model_spec& b) {
@@ -485,6 +487,8 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
 struct Launcher {
   fs_ensemble* e;
   hipStream_t s;
+  int group = -1, layer = -1, M = 0, N = 0, K = 0, Z = 1;
+  const char* kernel = "";
   template <class F>
   void operator()(int cls, double flops, double bytes, int launches, F&& fn) {
     if (!e->prof_on) {
@@ -501,7 +505,7 @@ struct Launcher {
       }
       return ev;
     };
-    ProfRec r{cls, take(), take(), flops, bytes, launches};
+    ProfRec r{cls, take(), take(), flops, bytes, launches, group, layer, M, N, K, Z, kernel};
     HIPCHK(hipEventRecord(r.a, s));
     fn();
     HIPCHK(hipEventRecord(r.b, s));
@@ -543,8 +547,14 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
   launch(K_PRE, 0.0, (double)B * oh * ow * 3 * esz, 1, [&] { launch_preprocess(pa, p, s); });
 
   char* arena = static_cast<char*>(e->arena.p);
-  for (Group& g : e->groups) {
-    for (LayerPlan& P : g.layers) {
+  for (size_t gi = 0; gi < e->groups.size(); ++gi) {
+    Group& g = e->groups[gi];
+    for (size_t li = 0; li < g.layers.size(); ++li) {
+      LayerPlan& P = g.layers[li];
+      launch.group = (int)gi;
+      launch.layer = (int)li;
+      launch.Z = g.Z;
+      launch.kernel = "";
       const void* x = P.in_slot == SLOT_INPUT ? e->input.p : slot_ptr(g, P.in_slot);
       const int64_t x_ms = P.in_slot == SLOT_INPUT ? 0 : (int64_t)g.slot_elems[P.in_slot] * Bm;
       void* y = nullptr;
@@ -571,6 +581,8 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           a.K = P.K; a.Kp = P.Kp; a.M = B * P.out.H * P.out.W; a.Z = g.Z;
           const int tile = conv_pick_tile(p, a, e->num_cus);
           if (tile < 0) fail(FS_ERR_INTERNAL, "no conv tile fits a planned layer");
+          launch.M = a.M; launch.N = a.Cout; launch.K = P.kh * P.kw * P.in.C;
+          launch.kernel = conv_tile(p, tile).name;
           const double kreal = (double)P.kh * P.kw * P.in.C;
           const double flops = 2.0 * a.M * a.Cout * kreal * g.Z;
           const double in_b = (double)B * P.in.H * P.in.W * P.in.C * esz * (P.in_slot == SLOT_INPUT ? 1 : g.Z);
@@ -601,6 +613,8 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           a.B = B; a.K = P.K; a.N = P.out.C; a.relu = P.relu; a.out_f32 = P.last ? 1 : 0;
           a.Z = g.Z;
           a.split = fc_pick_split(p, B, a.K, a.N, g.Z, e->num_cus);
+          launch.M = B; launch.N = a.N; launch.K = a.K;
+          launch.kernel = a.split > 1 ? "fc_splitk" : "fc";
           const double flops = 2.0 * B * a.N * (double)a.K * g.Z;
           const double bytes = ((double)a.N * a.K * esz + (double)B * a.K * esz +
                                 (double)B * a.N * (a.out_f32 ? 4 : esz)) * g.Z;
@@ -611,6 +625,8 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
     }
   }
 
+  launch.group = launch.layer = -1;
+  launch.kernel = "";
   SoftmaxArgs sa{};
   sa.logits = logits;
   sa.probs = d_probs;
@@ -716,7 +732,7 @@ void check_images(const fs_image* imgs, int B) {
     const fs_image& im = imgs[b];
     if (!im.data) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " has no data");
     if (im.h < 1 || im.w < 1) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " has zero size");
-    if (im.w > (1 << 20) / 3 || im.h > (1 << 20)) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " is too large");
+    if (im.w > 32768 || im.h > 32768) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " is larger than 32768 pixels a side");
     if (im.row_stride < 3 * im.w) fail(FS_ERR_INVALID, "image " + std::to_string(b) + " row_stride < 3*w");
   }
 }
@@ -908,6 +924,31 @@ fs_status fs_profile_read(fs_ensemble* e, fs_kernel_stat* stats, int32_t max_sta
   });
 }
 
+fs_status fs_profile_launches(fs_ensemble* e, fs_launch_stat* out, int32_t max_out, int32_t* n_out) {
+  if (!e || !out || !n_out) {
+    g_thread_error = "NULL argument";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    HIPCHK(hipSetDevice(e->device));
+    int n = 0;
+    for (ProfRec& r : e->prof) {
+      if (n >= max_out) break;
+      HIPCHK(hipEventSynchronize(r.b));
+      float ms = 0.f;
+      HIPCHK(hipEventElapsedTime(&ms, r.a, r.b));
+      fs_launch_stat& o = out[n++];
+      std::memset(&o, 0, sizeof(o));
+      std::snprintf(o.kclass, sizeof(o.kclass), "%s", kClassName[r.cls]);
+      std::snprintf(o.kernel, sizeof(o.kernel), "%s", r.kernel ? r.kernel : "");
+      o.group = r.group; o.layer = r.layer; o.M = r.M; o.N = r.N; o.K = r.K; o.Z = r.Z;
+      o.ms = ms; o.flops = r.flops; o.bytes = r.bytes;
+    }
+    *n_out = n;
+  });
+}
+
 // ---------------------------------------------------------- test entries
 fs_status fs_test_preprocess(const fs_image* imgs, int32_t B, int32_t out_h, int32_t out_w, const float mean[3],
                              const float std_[3], int32_t precision, float* out, int32_t device) {
@@ -954,8 +995,9 @@ fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t
     const int cin_p = Cin == 3 ? 4 : Cin;
     if (Cin != 3 && Cin % (p == BF16 ? 8 : 4)) fail(FS_ERR_UNSUPPORTED, "Cin must be 3 or a multiple of the vector width");
     const int Ho = (H + 2 * pad - kh) / stride + 1, Wo = (W + 2 * pad - kw) / stride + 1;
-    if ((int64_t)B * H * W * cin_p >= (int64_t(1) << 31) || (int64_t)B * Ho * Wo * Cout >= (int64_t(1) << 31))
-      fail(FS_ERR_UNSUPPORTED, "tensor too large");
+    if ((int64_t)B * H * W * cin_p * es(p) >= (int64_t(1) << 31) ||
+        (int64_t)B * Ho * Wo * Cout * es(p) >= (int64_t(1) << 31))
+      fail(FS_ERR_UNSUPPORTED, "tensor exceeds 2 GiB");
     set_device(device);
     TmpDev t;
     std::vector<float> xin;
@@ -1095,6 +1137,67 @@ fs_status fs_test_softmax_combine(const float* logits, int32_t N, int32_t B, int
     if (mean) HIPCHK(hipMemcpy(mean, dm, (size_t)B * C * 4, hipMemcpyDeviceToHost));
     HIPCHK(hipMemcpy(vote, dv, (size_t)B * 4, hipMemcpyDeviceToHost));
     if (top1) HIPCHK(hipMemcpy(top1, dt, (size_t)N * B * 4, hipMemcpyDeviceToHost));
+  });
+}
+
+fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Cout, int32_t kh, int32_t kw,
+                        int32_t stride, int32_t pad, int32_t relu, int32_t residual, int32_t precision, int32_t tile,
+                        int32_t Z, int32_t iters, double* avg_ms, int32_t* tile_used, int32_t device) {
+  return guarded(nullptr, [&] {
+    Prec p = prec_of(precision);
+    if (!avg_ms || B < 1 || H < 1 || W < 1 || Cin < 1 || Cout < 1 || kh < 1 || kw < 1 || stride < 1 || pad < 0 ||
+        Z < 1 || iters < 1)
+      fail(FS_ERR_INVALID, "bad bench arguments");
+    if (H + 2 * pad < kh || W + 2 * pad < kw) fail(FS_ERR_INVALID, "conv output would be empty");
+    if (Cout % 8) fail(FS_ERR_UNSUPPORTED, "Cout must be a multiple of 8");
+    const int cin_p = Cin == 3 ? 4 : Cin;
+    if (Cin != 3 && Cin % (p == BF16 ? 8 : 4)) fail(FS_ERR_UNSUPPORTED, "Cin must be 3 or a multiple of the vector width");
+    const int Ho = (H + 2 * pad - kh) / stride + 1, Wo = (W + 2 * pad - kw) / stride + 1;
+    const int64_t nx = (int64_t)B * H * W * cin_p, ny = (int64_t)B * Ho * Wo * Cout;
+    if (nx * es(p) >= (int64_t(1) << 31) || ny * es(p) >= (int64_t(1) << 31))
+      fail(FS_ERR_UNSUPPORTED, "tensor exceeds 2 GiB");
+    set_device(device);
+    const int K = kh * kw * cin_p, Kp = (int)round_up(K, CONV_KPAD);
+    TmpDev t;
+    const size_t e = es(p);
+    void* dx = t.alloc(nx * e);
+    void* dw = t.alloc((size_t)Z * Cout * Kp * e);
+    void* db = t.alloc((size_t)Z * Cout * 4);
+    void* dr = residual ? t.alloc((size_t)Z * ny * e) : nullptr;
+    void* dy = t.alloc((size_t)Z * ny * e);
+    // small finite values everywhere (0x3c00 = 2^-7 in bf16)
+    HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dx), 0x3c00, nx * e / 2));
+    HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dw), 0x3c00, (size_t)Z * Cout * Kp * e / 2));
+    HIPCHK(hipMemset(db, 0, (size_t)Z * Cout * 4));
+    if (dr) HIPCHK(hipMemset(dr, 0, (size_t)Z * ny * e));
+    ConvArgs a{};
+    a.x = dx; a.x_mstride = 0;
+    a.w = dw; a.w_mstride = (int64_t)Cout * Kp;
+    a.bias = static_cast<const float*>(db); a.b_mstride = Cout;
+    a.res = dr; a.res_mstride = ny;
+    a.y = dy; a.y_mstride = ny;
+    a.B = B; a.H = H; a.W = W; a.Cin = cin_p; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
+    a.kh = kh; a.kw = kw; a.stride = stride; a.pad = pad; a.relu = relu ? 1 : 0;
+    a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = Z;
+    int tl = tile < 0 ? conv_pick_tile(p, a, num_cus_of(device)) : tile;
+    if (!conv_tile_ok(p, tl, a)) fail(FS_ERR_UNSUPPORTED, "tile does not fit this conv");
+    if (tile_used) *tile_used = tl;
+    hipStream_t s = nullptr;
+    for (int i = 0; i < 3; ++i) launch_conv(a, p, tl, s);
+    HIPCHK(hipGetLastError());
+    hipEvent_t e0, e1;
+    HIPCHK(hipEventCreate(&e0));
+    HIPCHK(hipEventCreate(&e1));
+    HIPCHK(hipEventRecord(e0, s));
+    for (int i = 0; i < iters; ++i) launch_conv(a, p, tl, s);
+    HIPCHK(hipEventRecord(e1, s));
+    HIPCHK(hipEventSynchronize(e1));
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, e0, e1));
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    HIPCHK(hipGetLastError());
+    *avg_ms = ms / iters;
   });
 }
 

@@ -81,6 +81,13 @@ class fs_kernel_stat(ctypes.Structure):
                 ("bytes", ctypes.c_double)]
 
 
+class fs_launch_stat(ctypes.Structure):
+    _fields_ = [("kclass", ctypes.c_char * 16), ("kernel", ctypes.c_char * 32),
+                ("group", ctypes.c_int32), ("layer", ctypes.c_int32), ("M", ctypes.c_int32),
+                ("N", ctypes.c_int32), ("K", ctypes.c_int32), ("Z", ctypes.c_int32),
+                ("ms", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
 # every symbol include/flexserve.h declares: (name, restype, argtypes)
 SIGNATURES = [
     ("fs_ensemble_create", ctypes.c_int, [ctypes.POINTER(fs_ensemble_desc), ctypes.POINTER(_vp)]),
@@ -91,6 +98,7 @@ SIGNATURES = [
     ("fs_query", ctypes.c_int, [_vp, ctypes.POINTER(fs_info)]),
     ("fs_profile_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
+    ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
                                           ctypes.c_int32, _fp, _fp, ctypes.c_int32, _fp, ctypes.c_int32]),
     ("fs_test_conv", ctypes.c_int, [_fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -103,6 +111,8 @@ SIGNATURES = [
                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _fp, ctypes.c_int32]),
     ("fs_test_softmax_combine", ctypes.c_int, [_fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                _fp, _fp, _i32p, _i32p, ctypes.c_int32]),
+    ("fs_bench_conv", ctypes.c_int, [ctypes.c_int32] * 15 + [ctypes.POINTER(ctypes.c_double), _i32p,
+                                                         ctypes.c_int32]),
     ("fs_conv_num_tiles", ctypes.c_int32, [ctypes.c_int32]),
     ("fs_conv_tile_name", ctypes.c_char_p, [ctypes.c_int32, ctypes.c_int32]),
 ]
@@ -270,6 +280,18 @@ def fs_profile_read(handle) -> dict:
             for i in range(n.value)}
 
 
+def fs_profile_launches(handle, max_out=4096) -> list:
+    out = (fs_launch_stat * max_out)()
+    n = ctypes.c_int32()
+    _check(load().fs_profile_launches(handle, out, max_out, ctypes.byref(n)), handle)
+    res = []
+    for i in range(n.value):
+        r = out[i]
+        res.append(dict(kclass=r.kclass.decode(), kernel=r.kernel.decode(), group=r.group, layer=r.layer,
+                        M=r.M, N=r.N, K=r.K, Z=r.Z, ms=r.ms, flops=r.flops, bytes=r.bytes))
+    return res
+
+
 def fs_test_preprocess(imgs, out_h, out_w, mean, std, precision, device=0):
     B = len(imgs)
     out = np.zeros((B, out_h, out_w, 4), np.float32)
@@ -332,6 +354,17 @@ def fs_test_softmax_combine(logits, device=0):
     top1 = np.zeros((N, B), np.int32)
     _check(load().fs_test_softmax_combine(_f(z), N, B, C, _f(probs), _f(mean), _i(vote), _i(top1), device))
     return dict(probs=probs, mean=mean, vote=vote, top1=top1)
+
+
+def fs_bench_conv(B, H, W, Cin, Cout, k, stride, pad, relu=1, residual=0, precision=FS_BF16, tile=-1,
+                  Z=1, iters=20, device=0):
+    """Mean time (ms) of one launch of the conv kernel on this shape, and the
+    tile used."""
+    ms = ctypes.c_double()
+    used = ctypes.c_int32()
+    _check(load().fs_bench_conv(B, H, W, Cin, Cout, k, k, stride, pad, relu, residual, precision, tile, Z,
+                                iters, ctypes.byref(ms), ctypes.byref(used), device))
+    return ms.value, used.value
 
 
 def fs_conv_num_tiles(precision) -> int:

@@ -11,6 +11,13 @@ bf16 storage:   compared with the oracle in bf16-storage mode.
                 logits can each move by 3e-2*std); top-1 agreement >= 99.5%;
                 vote identical where the S margin exceeds 2*N*2e-2, else the
                 GPU vote lies within 2*N*2e-2 of the oracle's maximum of S.
+
+The oracle's own noise floor: when the oracle is rerun with fp32 sequential
+accumulation (o32), the difference nu from its double-accumulation run is
+what a change of summation order alone does to that row (bf16 storage makes
+random ResNets chaotic: one flipped bf16 rounding early moves late logits).
+A row whose nu exceeds the gate cannot be resolved by it; its gates widen to
+2*nu (probabilities, logits) and its top-1 exemption margin to 4*nu.
 """
 import numpy as np
 
@@ -30,7 +37,16 @@ def _top2_margin(v):
     return s[-1] - s[-2] if v.size > 1 else np.inf
 
 
-def compare(g, o, prec, idx=None, report=None):
+def oracle_acc32(models, imgs, out_hw, mean, std, prec, prepared=None):
+    """The oracle rerun with fp32 sequential accumulation (noise floor)."""
+    oracle.set_acc32(True)
+    try:
+        return oracle.ensemble(models, imgs, out_hw, mean, std, prec, prepared)
+    finally:
+        oracle.set_acc32(False)
+
+
+def compare(g, o, prec, idx=None, report=None, o32=None):
     """g: GPU outputs over the whole batch; o: oracle outputs for images idx
     (all when None).  Raises AssertionError with a description."""
     t = TOL[prec]
@@ -40,19 +56,31 @@ def compare(g, o, prec, idx=None, report=None):
     gv, gt = g["vote"][sel], g["top1"][:, sel]
     op, oz, ov, ot, oS = o["probs"], o["logits"], o["vote"], o["top1"], o["S"]
     dp = np.abs(gp - op).max()
-    assert dp <= t["p"], f"max |dp| = {dp:.3g} > {t['p']}"
-    agree, total, exempt = 0, 0, 0
+    agree, total, exempt, widened = 0, 0, 0, 0
     worst_rel = 0.0
+    nu_p_max = 0.0
+    gate_img = np.full(op.shape[1], t["p"])
     for i in range(N):
         for b in range(op.shape[1]):
             sd = float(np.std(oz[i, b]))
+            nu_p = nu_z = 0.0
+            if o32 is not None:
+                nu_p = float(np.abs(o32["probs"][i, b] - op[i, b]).max())
+                nu_z = float(np.abs(o32["logits"][i, b] - oz[i, b]).max())
+                nu_p_max = max(nu_p_max, nu_p)
+            dpr = float(np.abs(gp[i, b] - op[i, b]).max())
+            gate_p = max(t["p"], 2 * nu_p)
+            widened += int(gate_p > t["p"])
+            gate_img[b] = max(gate_img[b], gate_p)
+            assert dpr <= gate_p, f"model {i} image {b}: max |dp| = {dpr:.3g} > {gate_p:.3g} (nu {nu_p:.3g})"
             if t["logit_rel"] is not None:
                 rel = float(np.abs(gz[i, b] - oz[i, b]).max() / max(sd, 1e-30))
                 worst_rel = max(worst_rel, rel)
-                assert rel <= t["logit_rel"], f"model {i} image {b}: logit error {rel:.3g} of std"
-                thr = max(t["margin"], 2 * t["logit_rel"] * sd)
+                gate_z = max(t["logit_rel"], 2 * nu_z / max(sd, 1e-30))
+                assert rel <= gate_z, f"model {i} image {b}: logit error {rel:.3g} of std > {gate_z:.3g}"
+                thr = max(t["margin"], 2 * t["logit_rel"] * sd, 4 * nu_z)
             else:
-                thr = t["margin"]
+                thr = max(t["margin"], 4 * nu_z)
             total += 1
             agree += int(gt[i, b] == ot[i, b])
             if _top2_margin(oz[i, b]) > thr:
@@ -61,12 +89,12 @@ def compare(g, o, prec, idx=None, report=None):
                 exempt += 1
     if prec == "bf16":
         assert agree / total >= 0.995, f"top-1 agreement {agree}/{total}"
-    vt = 2 * N * t["vote"]
     for b in range(op.shape[1]):
+        vt = 2 * N * gate_img[b]
         if _top2_margin(oS[b]) > vt:
             assert gv[b] == ov[b], f"image {b}: vote {gv[b]} vs {ov[b]}"
         else:
             assert oS[b, gv[b]] >= oS[b].max() - vt, f"image {b}: vote {gv[b]} not near the maximum"
     if report is not None:
         report.update(max_dp=float(dp), top1_agree=agree / total, exempt=exempt,
-                      worst_logit_rel=worst_rel)
+                      worst_logit_rel=worst_rel, oracle_nu_p=nu_p_max, rows_widened=widened)

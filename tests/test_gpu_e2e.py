@@ -10,7 +10,7 @@ import pytest
 import oracle
 import workloads as wl
 from paper_2003_01538_amd import flexserve as fsb
-from tests.parity import compare
+from tests.parity import compare, oracle_acc32
 
 pytestmark = pytest.mark.gpu
 MEAN, STD = wl.IMAGENET_MEAN, wl.IMAGENET_STD
@@ -27,8 +27,13 @@ def _images(w):
 
 def _check(w, ens, imgs, sample, report=None):
     g = ens.infer(imgs)
-    o = oracle.ensemble(w["models"], [imgs[i] for i in sample], w["out_hw"], MEAN, STD, w["precision"])
-    compare(g, o, w["precision"], idx=sample, report=report)
+    sub = [imgs[i] for i in sample]
+    prepared = [oracle.prepare_model(m, w["precision"]) for m in w["models"]]
+    o = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, w["precision"], prepared)
+    o32 = None
+    if w["precision"] == "bf16":
+        o32 = oracle_acc32(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+    compare(g, o, w["precision"], idx=sample, report=report, o32=o32)
     return g
 
 

@@ -5,7 +5,8 @@ Tolerances (derived from the arithmetic):
 * fp32 storage: |gpu - oracle| <= 1e-5 * sum|x*w| + 1e-6 (an fp32 sum in
   another order against a double sum).
 * bf16 storage: |gpu - oracle| <= 1 bf16 ulp of the oracle value +
-  2^-16 * sum|x*w|, and at least 99% of the outputs bit-identical.
+  2^-16 * sum|x*w|, and at least 99% of the outputs bit-identical
+  (preprocess: + 2e-6 absolute for the cancellation in v/255 - mean).
 * max pool: bit-exact.  Softmax: 1e-6 absolute."""
 import numpy as np
 import pytest
@@ -26,9 +27,9 @@ def ulp_bf16(x):
     return np.float32(2.0) ** (e - 7)
 
 
-def assert_bf16_close(g, o, absacc=None, frac_exact=0.99, what=""):
+def assert_bf16_close(g, o, absacc=None, frac_exact=0.99, what="", abs_tol=0.0):
     g, o = np.asarray(g, np.float32), np.asarray(o, np.float32)
-    tol = ulp_bf16(o) + (0 if absacc is None else 2.0 ** -16 * absacc)
+    tol = ulp_bf16(o) + (0 if absacc is None else 2.0 ** -16 * absacc) + abs_tol
     bad = np.abs(g - o) > tol
     assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} outside 1 ulp + bound; max err {np.abs(g - o).max()}"
     exact = np.mean(g.view(np.uint32) == o.view(np.uint32))
@@ -60,7 +61,9 @@ def test_preprocess_parity(gpu_lib, prec, case):
         if prec == F32:
             assert np.max(np.abs(g[i, ..., :3] - o)) <= 1e-5, (case, i)
         else:
-            assert_bf16_close(g[i, ..., :3], o, frac_exact=0.99, what=f"{case}[{i}]")
+            # (v/255 - mean) cancels near zero: the fp32 kernel carries an
+            # absolute error of a few fp32 ulps of the operands (|x| <= 4.4)
+            assert_bf16_close(g[i, ..., :3], o, frac_exact=0.99, what=f"{case}[{i}]", abs_tol=2e-6)
 
 
 # ----------------------------------------------------------------------- conv
