@@ -183,11 +183,13 @@ fs_status fs_profile_launches(fs_ensemble *e, fs_launch_stat *out, int32_t max_o
  * tests).  precision selects fp32 or bf16 storage; in bf16 the inputs must
  * already be bf16-representable and outputs are returned widened to fp32. */
 
-/* Sec. 2.2 transformation of B host images into out [B][out_h][out_w][4]
- * (channel 3 is zero padding). */
+/* The shared transformation of B host images.  layout 0: out
+ * [B][out_h][out_w][4] (channel 3 is zero padding); layout 1 (bf16, even
+ * sizes): the space-to-depth form [B][out_h/2][out_w/2][16] whose channel
+ * (sy*2 + sx)*3 + c holds pixel (2Y + sy, 2X + sx), channel c (12..15 zero). */
 fs_status fs_test_preprocess(const fs_image *imgs, int32_t B, int32_t out_h, int32_t out_w,
                              const float mean[3], const float std_[3], int32_t precision,
-                             float *out, int32_t device);
+                             int32_t layout, float *out, int32_t device);
 
 /* Convolution with fused epilogue: out = relu?(conv(in, w) + bias + res).
  * in [B][H][W][Cin], w [Cout][kh][kw][Cin], bias [Cout] or NULL,

@@ -23,7 +23,10 @@ struct PreArgs {
   const ImageDesc* desc;
   int B, out_h, out_w;
   float mean[3], std_[3];
-  void* out;  // [B][out_h][out_w][4], bf16 or fp32
+  void* out;      // [B][out_h][out_w][4], bf16 or fp32, or null
+  void* out_s2d;  // bf16 [B][out_h/2][out_w/2][16] space-to-depth layout, or null:
+                  // channel (sy*2 + sx)*3 + c holds pixel (2Y+sy, 2X+sx), channel c;
+                  // channels 12..15 are zero
 };
 void launch_preprocess(const PreArgs& a, Prec p, hipStream_t s);
 
@@ -44,11 +47,15 @@ struct ConvArgs {
 struct ConvTile {
   int bm, bn, vec;   // block tile and A-load vector (elements)
   const char* name;
+  int dma = 0;       // 0: register-staged gather kernel; >0: LDS-DMA kernel with this many stages
+  int waves = 4;     // LDS-DMA kernel: waves per workgroup
 };
 int conv_num_tiles(Prec p);
 const ConvTile& conv_tile(Prec p, int t);
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a);
+bool conv_dma_ok(const ConvArgs& a);
+void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int stages, hipStream_t s);
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s);
 constexpr int CONV_KPAD = 64;  // packed reduction length is a multiple of this
 

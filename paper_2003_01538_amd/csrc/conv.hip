@@ -304,6 +304,13 @@ static const ConvTile kTilesBF16[] = {
     {128, 64, 4, "bf16_128x64_v4"},
     {64, 64, 4, "bf16_64x64_v4"},
     {256, 64, 8, "bf16_256x64_v8"},
+    {128, 128, 8, "bf16dma2_128x128_w4_v8", 2, 4},
+    {128, 64, 8, "bf16dma3_128x64_w4_v8", 3, 4},
+    {64, 128, 8, "bf16dma3_64x128_w4_v8", 3, 4},
+    {64, 64, 8, "bf16dma3_64x64_w4_v8", 3, 4},
+    {256, 128, 8, "bf16dma3_256x128_w8_v8", 3, 8},
+    {128, 256, 8, "bf16dma3_128x256_w8_v8", 3, 8},
+    {256, 64, 8, "bf16dma3_256x64_w8_v8", 3, 8},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -319,6 +326,7 @@ const ConvTile& conv_tile(Prec p, int t) { return p == BF16 ? kTilesBF16[t] : kT
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (t < 0 || t >= conv_num_tiles(p)) return false;
   const ConvTile& c = conv_tile(p, t);
+  if (c.dma) return p == BF16 && conv_dma_ok(a);
   return a.Cin % c.vec == 0 && a.Kp % CONV_KPAD == 0 && a.Cout % 8 == 0;
 }
 
@@ -336,7 +344,7 @@ int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus) {
     const double fill = wgs >= 2.0 * num_cus ? 1.0 : wgs / (2.0 * num_cus);
     const double reuse = (double)c.bm * c.bn / (c.bm + c.bn) / 64.0;  // 1.0 for 128x128
     const double score = useful * (0.35 + 0.65 * fill) * (0.6 + 0.4 * reuse) *
-                         (c.vec == 8 || p == F32 ? 1.0 : 0.9);
+                         (c.vec == 8 || p == F32 ? 1.0 : 0.9) * (c.dma ? 1.5 : 1.0);
     if (score > best_score) { best_score = score; best = t; }
   }
   return best;
@@ -352,6 +360,11 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
 }
 
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
+  if (p == BF16 && conv_tile(p, tile).dma) {
+    const ConvTile& c = conv_tile(p, tile);
+    launch_conv_dma(a, c.bm, c.bn, c.waves, c.dma, s);
+    return;
+  }
   if (p == BF16) {
     switch (tile) {
       case 0: launch_t<BF16, 128, 128, 8>(a, s); break;

@@ -1,0 +1,264 @@
+// Convolution as an implicit GEMM on the CDNA4 matrix cores, operands fed
+// to LDS by direct (LDS-DMA) buffer loads.
+//
+// Same GEMM view as the register-staged kernel (rows m = (b, oy, ox), columns
+// n = output channel, reduction k = (ky, kx, ci) with ci fastest) for layers
+// whose 64-wide K-tiles each lie in one filter row (Cin a multiple of 64, or
+// kw * Cin a multiple of 64 with Cin dividing 64): the tap is wave-uniform and
+// each tile row is one contiguous 128-byte run of input channels/pixels.
+//
+// Loads: `buffer_load_dwordx4 ... lds` writes lane j's 16 bytes to
+// LDS[M0 + 16 j] without touching VGPRs; offsets past the buffer read as
+// zero, which supplies the convolution's zero padding and the rows/columns
+// past M and N.  A wave instruction fills 8 tile rows (1 KB).  Rows are
+// stored unpadded with their eight 16-byte chunks XOR-swizzled by (row & 7),
+// so the 16 rows an MFMA operand read touches fall on distinct banks.
+//
+// Pipeline: STAGES LDS buffers.  Iteration k waits (vmcnt) for its own
+// wave's loads of tile k, meets the other waves at one barrier (after which
+// tile k is complete in LDS and tile k-1's buffer is free), issues the loads
+// of tile k + STAGES - 1, and runs the MFMAs of tile k.
+//
+// Four or eight waves per workgroup, v_mfma_f32_32x32x16_bf16 (on gfx950
+// it sustains ~1.4x the rate of the 16x16x32 form), fp32 accumulators; the
+// epilogue (bias, residual, ReLU, bf16 store) goes through
+// LDS for 16-byte coalesced rows.  One launch covers the Z models of a group.
+#include "common.hpp"
+#include "device.hpp"
+
+namespace fs {
+
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int BK = 64;          // bf16 elements per K-tile row (128 bytes)
+constexpr int ROW = 128;        // LDS bytes per tile row
+constexpr uint32_t OOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// BM x BN block tile, WGM x WGN waves (wave tile BM/WGM x BN/WGN, multiples
+// of 32), v_mfma_f32_32x32x16_bf16.
+template <int BM, int BN, int WGM, int WGN, int STAGES>
+__global__ void __launch_bounds__(64 * WGM * WGN,
+                                  (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
+  constexpr int NW = WGM * WGN, NTH = 64 * NW;
+  constexpr int TM = BM / WGM, TN = BN / WGN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int AP = BM / (8 * NW), BP = BN / (8 * NW);  // DMA instructions per wave per tile
+  constexpr int LPT = AP + BP;                             // vmcnt units per tile
+  constexpr int STAGE = (BM + BN) * ROW;
+  constexpr int CS = BM * (BN + 4) * 4;
+  constexpr int SMEM = STAGES * STAGE > CS ? STAGES * STAGE : CS;
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile");
+  static_assert(AP * 8 * NW == BM && BP * 8 * NW == BN, "DMA blocks");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.Cout + BN - 1) / BN;
+  const int tiles = tiles_m * tiles_n;
+  const int id = xcd_remap(blockIdx.x, tiles * a.Z);
+  const int z = id / tiles, tile = id - z * tiles;
+  const int mt = tile / tiles_n, ntile = tile - mt * tiles_n;
+  const int m0 = mt * BM, n0 = ntile * BN;
+
+  const __amdgpu_buffer_rsrc_t rx = rsrc(reinterpret_cast<const uint16_t*>(a.x) + z * a.x_mstride,
+                                         (uint32_t)((int64_t)a.B * a.H * a.W * a.Cin * 2));
+  const __amdgpu_buffer_rsrc_t rw = rsrc(reinterpret_cast<const uint16_t*>(a.w) + z * a.w_mstride,
+                                         (uint32_t)((int64_t)a.Cout * a.Kp * 2));
+
+  // lane j of a DMA instruction writes LDS row (j >> 3) of its 8-row block,
+  // physical chunk (j & 7), which holds logical chunk (j & 7) ^ (j >> 3)
+  const int lr = lane >> 3;
+  const int lc = (lane & 7) ^ lr;
+  // when Cin < 64 a 64-wide K-tile spans 64 / Cin consecutive pixels of one
+  // filter row: this lane's 8 channels belong to pixel kx + dx
+  const int dx = (lc * 8) / a.Cin;
+
+  int a_off[AP], a_iy[AP], a_ix[AP];
+  const int HoWo = a.Ho * a.Wo;
+#pragma unroll
+  for (int i = 0; i < AP; ++i) {
+    const int m = m0 + (i * NW + wave) * 8 + lr;
+    if (m < a.M) {
+      const int b = m / HoWo, r = m - b * HoWo;
+      const int oy = r / a.Wo, ox = r - oy * a.Wo;
+      a_iy[i] = oy * a.stride - a.pad;
+      a_ix[i] = ox * a.stride - a.pad;
+      a_off[i] = ((b * a.H + a_iy[i]) * a.W + a_ix[i]) * a.Cin + lc * 8;
+    } else {
+      a_iy[i] = -(1 << 28);
+      a_ix[i] = 0;
+      a_off[i] = 0;
+    }
+  }
+  uint32_t b_off[BP];
+#pragma unroll
+  for (int i = 0; i < BP; ++i) {
+    const int n = n0 + (i * NW + wave) * 8 + lr;
+    b_off[i] = n < a.Cout ? (uint32_t)((n * a.Kp + lc * 8) * 2) : OOB;
+  }
+
+  auto issue = [&](int kt, int stage) {
+    const int k0 = kt * BK;
+    const int tap = k0 / a.Cin;
+    const int ci0 = k0 - tap * a.Cin;
+    const int ky = tap / a.kw, kx = tap - ky * a.kw;
+    const int tap_off = (ky * a.W + kx) * a.Cin + ci0;
+    char* base = smem + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < AP; ++i) {
+      const int iy = a_iy[i] + ky, ix = a_ix[i] + kx + dx;
+      const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+      const uint32_t off = ok ? (uint32_t)((a_off[i] + tap_off) * 2) : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(base + (i * NW + wave) * 1024), 16, off, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < BP; ++i) {
+      const uint32_t off = b_off[i] == OOB ? OOB : b_off[i] + (uint32_t)(k0 * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void*)(base + BM * ROW + (i * NW + wave) * 1024), 16,
+                                               off, 0, 0, 0);
+    }
+  };
+
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // 32x32x16 operands: lane l supplies row (l & 31), k-group (l >> 5) of 8
+  const int fr = lane & 31, fq = lane >> 5;
+  auto compute = [&](int stage) {
+    const char* As = smem + stage * STAGE;
+    const char* Bs = As + BM * ROW;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {  // two halves of the 64-wide K-tile
+      bf16x8 af[2][FM], bfr[2][FN];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c = (kh * 2 + ks) * 2 + fq;  // logical 16-byte chunk
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int r = wm * TM + i * 32 + fr;
+          af[ks][i] = *reinterpret_cast<const bf16x8*>(As + r * ROW + ((c ^ (r & 7)) << 4));
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int r = wn * TN + j * 32 + fr;
+          bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + r * ROW + ((c ^ (r & 7)) << 4));
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  const int nk = a.Kp / BK;
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+  for (int kt = 0; kt < nk; ++kt) {
+    // tiles issued after kt that may stay in flight
+    const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
+    if constexpr (STAGES == 2) {
+      wait_vmcnt<0>();
+    } else if constexpr (STAGES == 3) {
+      if (ahead >= 1) wait_vmcnt<LPT>(); else wait_vmcnt<0>();
+    } else {
+      if (ahead >= 2) wait_vmcnt<2 * LPT>();
+      else if (ahead == 1) wait_vmcnt<LPT>();
+      else wait_vmcnt<0>();
+    }
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    compute(kt % STAGES);
+  }
+  __syncthreads();
+
+  // ---- epilogue: accumulators -> LDS -> coalesced rows.  32x32 result
+  // layout: lane l holds column (l & 31), rows 8g + 4(l >> 5) + r.
+  float* Cs = reinterpret_cast<float*>(smem);
+  constexpr int CSTR = BN + 4;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          Cs[(wm * TM + i * 32 + g * 8 + fq * 4 + r) * CSTR + wn * TN + j * 32 + fr] = acc[i][j][g * 4 + r];
+  __syncthreads();
+
+  const float* __restrict__ bias = a.bias + z * a.b_mstride;
+  const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
+  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
+  constexpr int CPR = BN / 8;
+  for (int idx = tid; idx < BM * CPR; idx += NTH) {
+    const int row = idx / CPR, c8 = idx - row * CPR;
+    const int m = m0 + row, n = n0 + c8 * 8;
+    if (m >= a.M || n >= a.Cout) continue;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = Cs[row * CSTR + c8 * 8 + e] + bias[n + e];
+    const int64_t o = (int64_t)m * a.Cout + n;
+    if (res) {
+      float r[8];
+      bf8_to_f8(*reinterpret_cast<const uint4*>(res + o), r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += r[e];
+    }
+    if (a.relu)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+    *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
+  }
+}
+
+}  // namespace
+
+// Every 64-wide K-tile must lie in one filter row and cover whole pixels.
+bool conv_dma_ok(const ConvArgs& a) {
+  const bool tiles_ok = a.Cin % BK == 0 || (a.Cin % 8 == 0 && BK % a.Cin == 0 && (a.kw * a.Cin) % BK == 0);
+  return tiles_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0;
+}
+
+void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int stages, hipStream_t s) {
+  const int tiles = ((a.M + bm - 1) / bm) * ((a.Cout + bn - 1) / bn) * a.Z;
+#define FS_DMA(BMv, BNv, WMv, WNv, Sv)                                                                   \
+  if (bm == BMv && bn == BNv && waves == WMv * WNv && stages == Sv) {                                    \
+    hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
+    return;                                                                                              \
+  }
+  FS_DMA(128, 128, 2, 2, 2)
+  FS_DMA(128, 64, 2, 2, 3)
+  FS_DMA(64, 128, 2, 2, 3)
+  FS_DMA(64, 64, 2, 2, 3)
+  FS_DMA(256, 128, 4, 2, 3)
+  FS_DMA(128, 256, 2, 4, 3)
+  FS_DMA(256, 64, 4, 2, 3)
+#undef FS_DMA
+}
+
+}  // namespace fs

@@ -4,7 +4,9 @@
 // neighbour clamped at the border), then (v/255 - mean)/std per channel,
 // written once as NHWC with the channel dimension padded to 4 (the padding
 // channel is 0) so that the first convolution loads one aligned 8- or
-// 16-byte vector per pixel.
+// 16-byte vector per pixel, and/or in a space-to-depth layout (2x2 pixel
+// blocks of 3 channels, padded to 16) that turns a stride-2 first
+// convolution into a stride-1 one with 64-element filter rows.
 //
 // One thread per output pixel, 256 consecutive pixels of one image per
 // workgroup: the stores are fully coalesced; the four taps are gathered
@@ -16,15 +18,9 @@
 
 namespace fs {
 
-template <bool BF16>
-__global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
-  const int b = blockIdx.y;
-  const int pix = blockIdx.x * 256 + threadIdx.x;
-  if (pix >= a.out_h * a.out_w) return;
-  const int oy = pix / a.out_w, ox = pix - oy * a.out_w;
-  const ImageDesc d = a.desc[b];
+// Transformed value of output pixel (oy, ox), channels 0..2, of image d.
+__device__ __forceinline__ void transform_pixel(const PreArgs& a, const ImageDesc& d, int oy, int ox, float* o) {
   const uint8_t* img = a.pixels + d.offset;
-
   // Source coordinate s = ((2o + 1) * in - out) / (2 * out), clamped at 0:
   // the integer part and the fraction come from exact integer arithmetic,
   // so only the fraction itself is rounded (relative error 2^-24).
@@ -38,10 +34,8 @@ __global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
   x0 = min(x0, d.w - 1);
   const int y1 = min(y0 + 1, d.h - 1), x1 = min(x0 + 1, d.w - 1);
   const float hy = 1.0f - ly, hx = 1.0f - lx;
-
   const uint8_t* r0 = img + (int64_t)y0 * d.row_stride;
   const uint8_t* r1 = img + (int64_t)y1 * d.row_stride;
-  float o[4];
 #pragma unroll
   for (int c = 0; c < 3; ++c) {
     float v00 = r0[x0 * 3 + c], v01 = r0[x1 * 3 + c];
@@ -49,6 +43,17 @@ __global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
     float v = hy * (hx * v00 + lx * v01) + ly * (hx * v10 + lx * v11);
     o[c] = (v / 255.0f - a.mean[c]) / a.std_[c];
   }
+}
+
+template <bool BF16>
+__global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
+  const int b = blockIdx.y;
+  const int pix = blockIdx.x * 256 + threadIdx.x;
+  if (pix >= a.out_h * a.out_w) return;
+  const int oy = pix / a.out_w, ox = pix - oy * a.out_w;
+  const ImageDesc d = a.desc[b];
+  float o[4];
+  transform_pixel(a, d, oy, ox, o);
   o[3] = 0.0f;
   const int64_t idx = ((int64_t)b * a.out_h * a.out_w + pix);
   if (BF16) {
@@ -60,12 +65,37 @@ __global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
   }
 }
 
+// Space-to-depth layout for a stride-2 first convolution: one thread per 2x2
+// block of output pixels, 32 bytes written.
+__global__ void __launch_bounds__(256) k_preprocess_s2d(PreArgs a) {
+  const int b = blockIdx.y;
+  const int hs = a.out_h / 2, ws = a.out_w / 2;
+  const int pix = blockIdx.x * 256 + threadIdx.x;
+  if (pix >= hs * ws) return;
+  const int Y = pix / ws, X = pix - Y * ws;
+  const ImageDesc d = a.desc[b];
+  float o[16];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) transform_pixel(a, d, 2 * Y + (s >> 1), 2 * X + (s & 1), o + 3 * s);
+#pragma unroll
+  for (int e = 12; e < 16; ++e) o[e] = 0.f;
+  uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.out_s2d) + ((int64_t)b * hs * ws + pix) * 16);
+  dst[0] = f8_to_bf8(o);
+  dst[1] = f8_to_bf8(o + 8);
+}
+
 void launch_preprocess(const PreArgs& a, Prec p, hipStream_t s) {
-  dim3 grid((a.out_h * a.out_w + 255) / 256, a.B);
-  if (p == BF16)
-    hipLaunchKernelGGL(k_preprocess<true>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(k_preprocess<false>, grid, dim3(256), 0, s, a);
+  if (a.out) {
+    dim3 grid((a.out_h * a.out_w + 255) / 256, a.B);
+    if (p == BF16)
+      hipLaunchKernelGGL(k_preprocess<true>, grid, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(k_preprocess<false>, grid, dim3(256), 0, s, a);
+  }
+  if (a.out_s2d) {
+    dim3 grid(((a.out_h / 2) * (a.out_w / 2) + 255) / 256, a.B);
+    hipLaunchKernelGGL(k_preprocess_s2d, grid, dim3(256), 0, s, a);
+  }
 }
 
 }  // namespace fs

@@ -16,7 +16,9 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <map>
 #include <memory>
 #include <mutex>
 #include <string>
@@ -114,6 +116,9 @@ struct LayerPlan {
   int64_t w_melems = 0, b_melems = 0;
   int in_slot = SLOT_INPUT, res_slot = -1, out_slot = -1;
   bool last = false;
+  bool s2d = false;       // first conv rewritten on the space-to-depth input
+  int kreal = 0;          // kh * kw * cin of the layer as specified (FLOP count)
+  int in_c_real = 0;      // input channels as specified (byte count)
 };
 
 struct Group {
@@ -149,12 +154,17 @@ struct fs_ensemble {
   DevBuf arena;
   size_t arena_bytes = 0;
   DevBuf input;     // [max_batch][out_h][out_w][4]
+  DevBuf input_s2d; // [max_batch][out_h/2][out_w/2][16] bf16
+  bool need_plain = false, need_s2d = false;
   DevBuf partial;   // fc split-K scratch
   DevBuf logits;    // [N][max_batch][C] fp32
   // host-path staging
   DevBuf d_pixels, d_desc, d_probs, d_mean, d_vote, d_top1;
   HostBuf h_pixels, h_desc, h_out;
   hipStream_t stream = nullptr;
+  // conv tile per (batch bucket) -> per group -> per layer, measured once
+  std::map<int, std::vector<std::vector<int>>> tiles;
+  bool tune = true;
   // profiler
   bool prof_on = false;
   std::vector<ProfRec> prof;
@@ -309,6 +319,55 @@ void pack_fc(const fs_layer& L, const Shape& in, Prec p, void* dst_w, float* dst
   }
 }
 
+// ------------------------------------------------------ space-to-depth stem
+// A k x k, stride-2, pad (k-1)/2 convolution of the 3-channel transformed
+// input equals a stride-1 convolution of its space-to-depth form (2x2 pixel
+// blocks, channel (sy*2 + sx)*3 + c, padded to 16): input row 2*oy + q maps
+// to block row oy + floor(q/2), sub-row q mod 2, for q = ky - (k-1)/2.
+struct S2dGeom {
+  int ks, pad;
+};
+int floor_div2(int v) { return v >= 0 ? v / 2 : -((-v + 1) / 2); }
+S2dGeom s2d_geom(int k) {
+  const int p = (k - 1) / 2;
+  const int lo = floor_div2(-p), hi = floor_div2(p);
+  return S2dGeom{hi - lo + 1, -lo};
+}
+bool s2d_eligible(const fs_layer& L, const fs_preprocess& pre, Prec prec) {
+  return prec == BF16 && L.op == FS_OP_CONV && L.src < 0 && L.cin == 3 && L.stride == 2 && L.kh == L.kw &&
+         (L.kh % 2) == 1 && L.pad == (L.kh - 1) / 2 && pre.out_h % 2 == 0 && pre.out_w % 2 == 0;
+}
+// w16[co][Ky][Kx][16] from w[co][ky][kx][3]; taps that fall outside the
+// original filter are zero.
+std::vector<float> s2d_weights(const fs_layer& L) {
+  const int k = L.kh, p = (k - 1) / 2;
+  const S2dGeom g = s2d_geom(k);
+  std::vector<float> w16((size_t)L.cout * g.ks * g.ks * 16, 0.f);
+  for (int co = 0; co < L.cout; ++co)
+    for (int Ky = 0; Ky < g.ks; ++Ky)
+      for (int Kx = 0; Kx < g.ks; ++Kx)
+        for (int sy = 0; sy < 2; ++sy)
+          for (int sx = 0; sx < 2; ++sx) {
+            const int ky = 2 * (Ky - g.pad) + sy + p, kx = 2 * (Kx - g.pad) + sx + p;
+            if (ky < 0 || ky >= k || kx < 0 || kx >= k) continue;
+            for (int c = 0; c < 3; ++c)
+              w16[(((size_t)co * g.ks + Ky) * g.ks + Kx) * 16 + (sy * 2 + sx) * 3 + c] =
+                  L.weight[(((size_t)co * k + ky) * k + kx) * 3 + c];
+          }
+  return w16;
+}
+// The s2d form of a layer: same output, weights in w16 (caller keeps it alive).
+fs_layer s2d_layer(const fs_layer& L, const std::vector<float>& w16) {
+  const S2dGeom g = s2d_geom(L.kh);
+  fs_layer q = L;
+  q.cin = 16;
+  q.kh = q.kw = g.ks;
+  q.stride = 1;
+  q.pad = g.pad;
+  q.weight = w16.data();
+  return q;
+}
+
 // ----------------------------------------------------------- planning
 void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
   const fs_model_spec& s = d->models[g.first];
@@ -337,12 +396,27 @@ void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
     P.relu = L.relu ? 1 : 0;
     P.flatten = L.flatten_nchw ? 1 : 0;
     P.last = i == n - 1;
+    P.in_c_real = P.in.C;
     switch (L.op) {
       case FS_OP_CONV:
         P.out = Shape{(P.in.H + 2 * L.pad - L.kh) / L.stride + 1, (P.in.W + 2 * L.pad - L.kw) / L.stride + 1, L.cout};
         P.K = L.kh * L.kw * P.cin_p;
         P.Kp = (int)round_up(P.K, CONV_KPAD);
-        e->flops_per_image += 2.0 * P.out.H * P.out.W * L.cout * (double)L.kh * L.kw * L.cin * g.Z;
+        P.kreal = L.kh * L.kw * L.cin;
+        e->flops_per_image += 2.0 * P.out.H * P.out.W * L.cout * (double)P.kreal * g.Z;
+        if (s2d_eligible(L, d->pre, e->prec)) {  // launch geometry of the s2d form
+          const S2dGeom sg = s2d_geom(L.kh);
+          P.s2d = true;
+          P.in = Shape{d->pre.out_h / 2, d->pre.out_w / 2, 16};
+          P.cin_p = 16;
+          P.kh = P.kw = sg.ks;
+          P.stride = 1;
+          P.pad = sg.pad;
+          P.K = P.Kp = sg.ks * sg.ks * 16;
+          e->need_s2d = true;
+        } else if (L.src < 0) {
+          e->need_plain = true;
+        }
         break;
       case FS_OP_MAXPOOL:
         P.out = Shape{(P.in.H + 2 * L.pad - L.kh) / L.stride + 1, (P.in.W + 2 * L.pad - L.kw) / L.stride + 1, P.in.C};
@@ -405,6 +479,7 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   e->max_batch = d->max_batch;
   e->pre = d->pre;
   e->device = d->device;
+  if (const char* t = std::getenv("FS_TUNE")) e->tune = std::atoi(t) != 0;
   // groups of consecutive structurally identical models
   for (int m = 0; m < e->N;) {
     int z = 1;
@@ -444,10 +519,14 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
         const fs_layer& L = d->models[g.first + z].layers[li];
         void* wdst = host.data() + P.w_off + (size_t)z * P.w_melems * esz;
         float* bdst = reinterpret_cast<float*>(host.data() + P.b_off + (size_t)z * P.b_melems * 4);
-        if (P.op == FS_OP_CONV)
+        if (P.op == FS_OP_CONV && P.s2d) {
+          const std::vector<float> w16 = s2d_weights(L);
+          pack_conv(s2d_layer(L, w16), P.cin_p, P.Kp, e->prec, wdst, bdst);
+        } else if (P.op == FS_OP_CONV) {
           pack_conv(L, P.cin_p, P.Kp, e->prec, wdst, bdst);
-        else
+        } else {
           pack_fc(L, P.in, e->prec, wdst, bdst);
+        }
       }
     }
   }
@@ -477,9 +556,10 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
         for (int B = 1; B <= Bm; ++B)
           pf_all = std::max(pf_all, fc_partial_floats(B, P.out.C, fc_pick_split(e->prec, B, P.K, P.out.C, g.Z, e->num_cus), g.Z));
   e->partial.alloc(round_up(std::max<size_t>(pf_all, 1) * 4, 256));
-  e->input.alloc(round_up((size_t)Bm * e->pre.out_h * e->pre.out_w * 4 * esz, 256));
+  if (e->need_plain) e->input.alloc(round_up((size_t)Bm * e->pre.out_h * e->pre.out_w * 4 * esz, 256));
+  if (e->need_s2d) e->input_s2d.alloc(round_up((size_t)Bm * e->pre.out_h * e->pre.out_w * 4 * 2, 256));
   e->logits.alloc(round_up((size_t)e->N * Bm * e->C * 4, 256));
-  ws += e->partial.bytes + e->input.bytes + e->logits.bytes;
+  ws += e->partial.bytes + e->input.bytes + e->input_s2d.bytes + e->logits.bytes;
   e->workspace_bytes = ws;
 }
 
@@ -524,6 +604,82 @@ void prof_clear(fs_ensemble* e) {
 // ------------------------------------------------------------ device pass
 void* slot_ptr(Group& g, int slot) { return g.slots[slot].p; }
 
+ConvArgs conv_args(fs_ensemble* e, Group& g, const LayerPlan& P, int B, void* y, int64_t y_ms) {
+  const int Bm = e->max_batch;
+  char* arena = static_cast<char*>(e->arena.p);
+  ConvArgs a{};
+  a.x = P.in_slot == SLOT_INPUT ? (P.s2d ? e->input_s2d.p : e->input.p) : slot_ptr(g, P.in_slot);
+  a.x_mstride = P.in_slot == SLOT_INPUT ? 0 : (int64_t)g.slot_elems[P.in_slot] * Bm;
+  a.w = arena + P.w_off; a.w_mstride = P.w_melems;
+  a.bias = reinterpret_cast<const float*>(arena + P.b_off); a.b_mstride = P.b_melems;
+  a.res = P.res_slot >= 0 ? slot_ptr(g, P.res_slot) : nullptr;
+  a.res_mstride = P.res_slot >= 0 ? (int64_t)g.slot_elems[P.res_slot] * Bm : 0;
+  a.y = y; a.y_mstride = y_ms;
+  a.B = B; a.H = P.in.H; a.W = P.in.W; a.Cin = P.cin_p;
+  a.Ho = P.out.H; a.Wo = P.out.W; a.Cout = P.out.C;
+  a.kh = P.kh; a.kw = P.kw; a.stride = P.stride; a.pad = P.pad; a.relu = P.relu;
+  a.K = P.K; a.Kp = P.Kp; a.M = B * P.out.H * P.out.W; a.Z = g.Z;
+  return a;
+}
+
+int batch_bucket(int B, int max_batch) {
+  int b = 1;
+  while (b < B) b <<= 1;
+  return std::min(b, max_batch);
+}
+
+// Conv tiles for one batch bucket.  With tuning on, every candidate tile
+// of a layer is timed (HIP events, two launches after a warm-up) on the
+// layer's own buffers and the fastest kept.  Candidates are restricted to one
+// kernel family per layer (the LDS-DMA family when it applies, the
+// register-staged family otherwise): within a family every tile sums each
+// output in the same order, so the choice never changes the results.
+const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_t s) {
+  const int bucket = batch_bucket(B, e->max_batch);
+  auto it = e->tiles.find(bucket);
+  if (it != e->tiles.end()) return it->second;
+  std::vector<std::vector<int>> choice(e->groups.size());
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (e->tune) {
+    HIPCHK(hipEventCreate(&e0));
+    HIPCHK(hipEventCreate(&e1));
+  }
+  for (size_t gi = 0; gi < e->groups.size(); ++gi) {
+    Group& g = e->groups[gi];
+    choice[gi].assign(g.layers.size(), -1);
+    for (size_t li = 0; li < g.layers.size(); ++li) {
+      LayerPlan& P = g.layers[li];
+      if (P.op != FS_OP_CONV) continue;
+      ConvArgs a = conv_args(e, g, P, bucket, slot_ptr(g, P.out_slot), (int64_t)g.slot_elems[P.out_slot] * e->max_batch);
+      bool any_dma = false;
+      for (int t = 0; t < conv_num_tiles(e->prec); ++t)
+        if (conv_tile_ok(e->prec, t, a) && conv_tile(e->prec, t).dma) any_dma = true;
+      int best = conv_pick_tile(e->prec, a, e->num_cus);
+      if (e->tune) {
+        float best_ms = 1e30f;
+        for (int t = 0; t < conv_num_tiles(e->prec); ++t) {
+          if (!conv_tile_ok(e->prec, t, a) || (conv_tile(e->prec, t).dma != 0) != any_dma) continue;
+          launch_conv(a, e->prec, t, s);
+          HIPCHK(hipEventRecord(e0, s));
+          launch_conv(a, e->prec, t, s);
+          launch_conv(a, e->prec, t, s);
+          HIPCHK(hipEventRecord(e1, s));
+          HIPCHK(hipEventSynchronize(e1));
+          float ms = 0.f;
+          HIPCHK(hipEventElapsedTime(&ms, e0, e1));
+          if (ms < best_ms) { best_ms = ms; best = t; }
+        }
+        HIPCHK(hipGetLastError());
+      }
+      if (best < 0) fail(FS_ERR_INTERNAL, "no conv tile fits a planned layer");
+      choice[gi][li] = best;
+    }
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  return e->tiles.emplace(bucket, std::move(choice)).first->second;
+}
+
 void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
               float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s) {
   Launcher launch{e, s};
@@ -543,10 +699,13 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
     pa.mean[c] = e->pre.mean[c];
     pa.std_[c] = e->pre.std[c];
   }
-  pa.out = e->input.p;
-  launch(K_PRE, 0.0, (double)B * oh * ow * 3 * esz, 1, [&] { launch_preprocess(pa, p, s); });
+  pa.out = e->need_plain ? e->input.p : nullptr;
+  pa.out_s2d = e->need_s2d ? e->input_s2d.p : nullptr;
+  launch(K_PRE, 0.0, (double)B * oh * ow * 3 * esz * ((e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0)),
+         (e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0), [&] { launch_preprocess(pa, p, s); });
 
   char* arena = static_cast<char*>(e->arena.p);
+  const std::vector<std::vector<int>>& tiles = tiles_for(e, B, s);
   for (size_t gi = 0; gi < e->groups.size(); ++gi) {
     Group& g = e->groups[gi];
     for (size_t li = 0; li < g.layers.size(); ++li) {
@@ -555,7 +714,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
       launch.layer = (int)li;
       launch.Z = g.Z;
       launch.kernel = "";
-      const void* x = P.in_slot == SLOT_INPUT ? e->input.p : slot_ptr(g, P.in_slot);
+      const void* x = P.in_slot == SLOT_INPUT ? (P.s2d ? e->input_s2d.p : e->input.p) : slot_ptr(g, P.in_slot);
       const int64_t x_ms = P.in_slot == SLOT_INPUT ? 0 : (int64_t)g.slot_elems[P.in_slot] * Bm;
       void* y = nullptr;
       int64_t y_ms = 0;
@@ -568,24 +727,14 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
       }
       switch (P.op) {
         case FS_OP_CONV: {
-          ConvArgs a{};
-          a.x = x; a.x_mstride = x_ms;
-          a.w = arena + P.w_off; a.w_mstride = P.w_melems;
-          a.bias = reinterpret_cast<const float*>(arena + P.b_off); a.b_mstride = P.b_melems;
-          a.res = P.res_slot >= 0 ? slot_ptr(g, P.res_slot) : nullptr;
-          a.res_mstride = P.res_slot >= 0 ? (int64_t)g.slot_elems[P.res_slot] * Bm : 0;
-          a.y = y; a.y_mstride = y_ms;
-          a.B = B; a.H = P.in.H; a.W = P.in.W; a.Cin = P.cin_p;
-          a.Ho = P.out.H; a.Wo = P.out.W; a.Cout = P.out.C;
-          a.kh = P.kh; a.kw = P.kw; a.stride = P.stride; a.pad = P.pad; a.relu = P.relu;
-          a.K = P.K; a.Kp = P.Kp; a.M = B * P.out.H * P.out.W; a.Z = g.Z;
-          const int tile = conv_pick_tile(p, a, e->num_cus);
-          if (tile < 0) fail(FS_ERR_INTERNAL, "no conv tile fits a planned layer");
-          launch.M = a.M; launch.N = a.Cout; launch.K = P.kh * P.kw * P.in.C;
+          const ConvArgs a = conv_args(e, g, P, B, y, y_ms);
+          const int tile = tiles[gi][li];
+          launch.M = a.M; launch.N = a.Cout; launch.K = P.kreal;
           launch.kernel = conv_tile(p, tile).name;
-          const double kreal = (double)P.kh * P.kw * P.in.C;
+          const double kreal = (double)P.kreal;
           const double flops = 2.0 * a.M * a.Cout * kreal * g.Z;
-          const double in_b = (double)B * P.in.H * P.in.W * P.in.C * esz * (P.in_slot == SLOT_INPUT ? 1 : g.Z);
+          const double in_b = (double)B * P.in.H * P.in.W * P.in_c_real * (P.s2d ? 4 : 1) * esz *
+                              (P.in_slot == SLOT_INPUT ? 1 : g.Z);
           const double bytes = in_b + ((double)a.Cout * kreal * esz + (double)a.M * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
           launch(K_CONV, flops, bytes, 1, [&] { launch_conv(a, p, tile, s); });
           break;
@@ -642,7 +791,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
 }
 
 int launches_per_pass(fs_ensemble* e) {
-  int n = 2;  // preprocess + softmax/combine
+  int n = 1 + (e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0);  // preprocess + softmax/combine
   for (Group& g : e->groups)
     for (LayerPlan& P : g.layers)
       n += P.op == FS_OP_FC ? fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus)) : 1;
@@ -951,12 +1100,15 @@ fs_status fs_profile_launches(fs_ensemble* e, fs_launch_stat* out, int32_t max_o
 
 // ---------------------------------------------------------- test entries
 fs_status fs_test_preprocess(const fs_image* imgs, int32_t B, int32_t out_h, int32_t out_w, const float mean[3],
-                             const float std_[3], int32_t precision, float* out, int32_t device) {
+                             const float std_[3], int32_t precision, int32_t layout, float* out, int32_t device) {
   return guarded(nullptr, [&] {
     Prec p = prec_of(precision);
     check_images(imgs, B);
     if (B == 0) return;
     if (out_h < 1 || out_w < 1 || !mean || !std_ || !out) fail(FS_ERR_INVALID, "bad preprocess arguments");
+    if (layout != 0 && layout != 1) fail(FS_ERR_INVALID, "layout must be 0 (NHWC4) or 1 (space-to-depth)");
+    if (layout == 1 && (p != BF16 || out_h % 2 || out_w % 2))
+      fail(FS_ERR_UNSUPPORTED, "space-to-depth output needs bf16 and an even output size");
     set_device(device);
     TmpDev t;
     const size_t pb = packed_size(imgs, 0, B);
@@ -974,7 +1126,8 @@ fs_status fs_test_preprocess(const fs_image* imgs, int32_t B, int32_t out_h, int
     a.desc = static_cast<const ImageDesc*>(dd);
     a.B = B; a.out_h = out_h; a.out_w = out_w;
     for (int c = 0; c < 3; ++c) { a.mean[c] = mean[c]; a.std_[c] = std_[c]; }
-    a.out = dout;
+    a.out = layout == 0 ? dout : nullptr;
+    a.out_s2d = layout == 1 ? dout : nullptr;
     launch_preprocess(a, p, nullptr);
     HIPCHK(hipGetLastError());
     HIPCHK(hipDeviceSynchronize());
@@ -1000,21 +1153,41 @@ fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t
       fail(FS_ERR_UNSUPPORTED, "tensor exceeds 2 GiB");
     set_device(device);
     TmpDev t;
-    std::vector<float> xin;
+    fs_layer L{};
+    L.op = FS_OP_CONV; L.src = -1; L.cin = Cin; L.cout = Cout; L.kh = kh; L.kw = kw; L.stride = stride; L.pad = pad;
+    L.weight = w; L.bias = bias;
+    fs_preprocess pre{};
+    pre.out_h = H; pre.out_w = W;
+    // the space-to-depth form whenever the requested tile cannot gather
+    // 4-channel pixels (as the ensemble does for a stride-2 first conv)
+    const bool use_s2d = s2d_eligible(L, pre, p) && (tile < 0 || conv_tile(p, tile).vec == 8);
+    std::vector<float> xin, w16;
     const float* xsrc = in;
-    if (cin_p != Cin) {  // pad the channel dimension with zeros
+    int gH = H, gW = W, gC = cin_p, gk = kh, gs = stride, gp = pad;
+    if (use_s2d) {
+      gH = H / 2; gW = W / 2; gC = 16;
+      xin.assign((size_t)B * gH * gW * 16, 0.f);
+      for (int b = 0; b < B; ++b)
+        for (int y = 0; y < H; ++y)
+          for (int x = 0; x < W; ++x)
+            for (int c = 0; c < 3; ++c)
+              xin[(((size_t)b * gH + y / 2) * gW + x / 2) * 16 + ((y & 1) * 2 + (x & 1)) * 3 + c] =
+                  in[(((size_t)b * H + y) * W + x) * 3 + c];
+      xsrc = xin.data();
+      w16 = s2d_weights(L);
+      L = s2d_layer(L, w16);
+      gk = L.kh; gs = 1; gp = L.pad;
+    } else if (cin_p != Cin) {  // pad the channel dimension with zeros
       xin.assign((size_t)B * H * W * cin_p, 0.f);
       for (int64_t px = 0; px < (int64_t)B * H * W; ++px)
         for (int c = 0; c < Cin; ++c) xin[px * cin_p + c] = in[px * Cin + c];
       xsrc = xin.data();
     }
-    void* dx = upload_as(t, xsrc, (int64_t)B * H * W * cin_p, p);
-    fs_layer L{};
-    L.op = FS_OP_CONV; L.cin = Cin; L.cout = Cout; L.kh = kh; L.kw = kw; L.weight = w; L.bias = bias;
-    const int K = kh * kw * cin_p, Kp = (int)round_up(K, CONV_KPAD);
+    void* dx = upload_as(t, xsrc, (int64_t)B * gH * gW * gC, p);
+    const int K = gk * gk * gC, Kp = (int)round_up(K, CONV_KPAD);
     std::vector<char> wp((size_t)Cout * Kp * es(p));
     std::vector<float> bp(Cout);
-    pack_conv(L, cin_p, Kp, p, wp.data(), bp.data());
+    pack_conv(L, gC, Kp, p, wp.data(), bp.data());
     void* dw = t.alloc(wp.size());
     HIPCHK(hipMemcpy(dw, wp.data(), wp.size(), hipMemcpyHostToDevice));
     void* db = t.alloc(Cout * 4);
@@ -1024,8 +1197,8 @@ fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t
     void* dy = t.alloc(no * es(p));
     ConvArgs a{};
     a.x = dx; a.w = dw; a.bias = static_cast<const float*>(db); a.res = dr; a.y = dy;
-    a.B = B; a.H = H; a.W = W; a.Cin = cin_p; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
-    a.kh = kh; a.kw = kw; a.stride = stride; a.pad = pad; a.relu = relu ? 1 : 0;
+    a.B = B; a.H = gH; a.W = gW; a.Cin = gC; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
+    a.kh = gk; a.kw = gk; a.stride = gs; a.pad = gp; a.relu = relu ? 1 : 0;
     a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = 1;
     int tl = tile;
     if (tl < 0) tl = conv_pick_tile(p, a, num_cus_of(device));
@@ -1157,16 +1330,26 @@ fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Co
     if (nx * es(p) >= (int64_t(1) << 31) || ny * es(p) >= (int64_t(1) << 31))
       fail(FS_ERR_UNSUPPORTED, "tensor exceeds 2 GiB");
     set_device(device);
-    const int K = kh * kw * cin_p, Kp = (int)round_up(K, CONV_KPAD);
+    fs_layer L{};
+    L.op = FS_OP_CONV; L.src = -1; L.cin = Cin; L.cout = Cout; L.kh = kh; L.kw = kw; L.stride = stride; L.pad = pad;
+    fs_preprocess pre{};
+    pre.out_h = H; pre.out_w = W;
+    int gH = H, gW = W, gC = cin_p, gk = kh, gs = stride, gp = pad;
+    if (s2d_eligible(L, pre, p) && (tile < 0 || conv_tile(p, tile).vec == 8)) {
+      const S2dGeom g = s2d_geom(kh);
+      gH = H / 2; gW = W / 2; gC = 16; gk = g.ks; gs = 1; gp = g.pad;
+    }
+    const int K = gk * gk * gC, Kp = (int)round_up(K, CONV_KPAD);
+    const int64_t nxg = (int64_t)B * gH * gW * gC;
     TmpDev t;
     const size_t e = es(p);
-    void* dx = t.alloc(nx * e);
+    void* dx = t.alloc(nxg * e);
     void* dw = t.alloc((size_t)Z * Cout * Kp * e);
     void* db = t.alloc((size_t)Z * Cout * 4);
     void* dr = residual ? t.alloc((size_t)Z * ny * e) : nullptr;
     void* dy = t.alloc((size_t)Z * ny * e);
     // small finite values everywhere (0x3c00 = 2^-7 in bf16)
-    HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dx), 0x3c00, nx * e / 2));
+    HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dx), 0x3c00, nxg * e / 2));
     HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dw), 0x3c00, (size_t)Z * Cout * Kp * e / 2));
     HIPCHK(hipMemset(db, 0, (size_t)Z * Cout * 4));
     if (dr) HIPCHK(hipMemset(dr, 0, (size_t)Z * ny * e));
@@ -1176,8 +1359,8 @@ fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Co
     a.bias = static_cast<const float*>(db); a.b_mstride = Cout;
     a.res = dr; a.res_mstride = ny;
     a.y = dy; a.y_mstride = ny;
-    a.B = B; a.H = H; a.W = W; a.Cin = cin_p; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
-    a.kh = kh; a.kw = kw; a.stride = stride; a.pad = pad; a.relu = relu ? 1 : 0;
+    a.B = B; a.H = gH; a.W = gW; a.Cin = gC; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
+    a.kh = gk; a.kw = gk; a.stride = gs; a.pad = gp; a.relu = relu ? 1 : 0;
     a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = Z;
     int tl = tile < 0 ? conv_pick_tile(p, a, num_cus_of(device)) : tile;
     if (!conv_tile_ok(p, tl, a)) fail(FS_ERR_UNSUPPORTED, "tile does not fit this conv");

@@ -100,7 +100,8 @@ SIGNATURES = [
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
     ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
-                                          ctypes.c_int32, _fp, _fp, ctypes.c_int32, _fp, ctypes.c_int32]),
+                                          ctypes.c_int32, _fp, _fp, ctypes.c_int32, ctypes.c_int32, _fp,
+                                          ctypes.c_int32]),
     ("fs_test_conv", ctypes.c_int, [_fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                     _fp, _fp, _fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -292,13 +293,14 @@ def fs_profile_launches(handle, max_out=4096) -> list:
     return res
 
 
-def fs_test_preprocess(imgs, out_h, out_w, mean, std, precision, device=0):
+def fs_test_preprocess(imgs, out_h, out_w, mean, std, precision, layout=0, device=0):
     B = len(imgs)
-    out = np.zeros((B, out_h, out_w, 4), np.float32)
+    shape = (B, out_h, out_w, 4) if layout == 0 else (B, out_h // 2, out_w // 2, 16)
+    out = np.zeros(shape, np.float32)
     arr, keep = image_array(imgs)
     m = np.asarray(mean, np.float32)
     s = np.asarray(std, np.float32)
-    _check(load().fs_test_preprocess(arr, B, out_h, out_w, _f(m), _f(s), precision, _f(out), device))
+    _check(load().fs_test_preprocess(arr, B, out_h, out_w, _f(m), _f(s), precision, layout, _f(out), device))
     return out
 
 

@@ -127,5 +127,9 @@ def test_test_entries_validate_before_device():
     with pytest.raises(fsb.FsError) as e:
         fsb.fs_test_preprocess(bad, 8, 8, wl.IMAGENET_MEAN, wl.IMAGENET_STD, fsb.FS_F32)
     assert e.value.status == fsb.FS_ERR_INVALID
+    ok = [np.zeros((4, 4, 3), np.uint8)]
+    with pytest.raises(fsb.FsError) as e:  # space-to-depth needs an even size
+        fsb.fs_test_preprocess(ok, 7, 8, wl.IMAGENET_MEAN, wl.IMAGENET_STD, fsb.FS_BF16, layout=1)
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
     assert lib.fs_conv_num_tiles(fsb.FS_BF16) >= 3 and lib.fs_conv_num_tiles(9) == 0
     assert fsb.fs_conv_tile_name(fsb.FS_BF16, 0) and fsb.fs_conv_tile_name(fsb.FS_BF16, 99) is None

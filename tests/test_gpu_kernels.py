@@ -66,6 +66,17 @@ def test_preprocess_parity(gpu_lib, prec, case):
             assert_bf16_close(g[i, ..., :3], o, frac_exact=0.99, what=f"{case}[{i}]", abs_tol=2e-6)
 
 
+def test_preprocess_space_to_depth_layout(gpu_lib):
+    imgs = wl.images_ragged(4000, 3) + [wl.images_uniform(5, 1, 224, 224)[0]]
+    g = fsb.fs_test_preprocess(imgs, 224, 224, MEAN, STD, BF16, layout=1)
+    assert g.shape == (4, 112, 112, 16) and np.all(g[..., 12:] == 0)
+    for i, im in enumerate(imgs):
+        o = oracle.preprocess(im, 224, 224, MEAN, STD, "bf16")
+        # channel (sy*2 + sx)*3 + c of block (Y, X) is pixel (2Y+sy, 2X+sx), channel c
+        r = o.reshape(112, 2, 112, 2, 3).transpose(0, 2, 1, 3, 4).reshape(112, 112, 12)
+        assert_bf16_close(g[i, ..., :12], r, frac_exact=0.99, what=f"s2d[{i}]", abs_tol=2e-6)
+
+
 # ----------------------------------------------------------------------- conv
 CONV_CASES = [
     # B, H, W, Cin, Cout, k, stride, pad, relu, residual
@@ -114,12 +125,21 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
     o, ab = oracle.conv2d(x, w, b, s, p, relu, r, PREC[prec], want_abs=True)
     tiles = _tiles_for(prec, Cin)
     assert tiles
+    ran = 0
     for t in tiles + [-1]:
-        g = fsb.fs_test_conv(x, w, b, r, s, p, relu, prec, tile=t)
+        try:
+            g = fsb.fs_test_conv(x, w, b, r, s, p, relu, prec, tile=t)
+        except fsb.FsError as e:  # a tile that does not fit this shape (e.g. LDS-DMA needs Cin % 64 == 0)
+            assert e.status == fsb.FS_ERR_UNSUPPORTED and t >= 0
+            continue
+        ran += 1
         if prec == BF16:
             assert_bf16_close(g, o, ab, what=f"case {ci} tile {t}")
         else:
             assert np.all(np.abs(g - o) <= 1e-5 * ab + 1e-6), f"case {ci} tile {t}: {np.abs(g - o).max()}"
+    assert ran >= 2
+    if prec == BF16 and Cin % 64 == 0:  # the LDS-DMA kernels ran on this shape
+        assert ran >= 2 + sum(1 for t in tiles if "dma" in fsb.fs_conv_tile_name(prec, t))
 
 
 def test_conv_repeat_is_bit_identical(gpu_lib):
