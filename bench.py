@@ -38,9 +38,37 @@ def parse():
                     help="bound on the CPU-oracle sample (0 disables it)")
     ap.add_argument("--dump-launches", default="",
                     help="write the per-launch event times of one profiled step to this JSON file")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (scales the HBM byte "
+                         "counters of a profiler run) and exit")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
+
+
+PROFILE = os.path.join(ROOT, "profiles", "conv_resnet18x3_b32.md")
+
+
+def conv_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("conv.hip", "conv_dma.hip"):
+        with open(os.path.join(ROOT, "paper_2003_01538_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counted_traffic():
+    """HBM bytes per conv launch from the committed rocprofv3 counter summary,
+    or None when the conv sources changed since the counters were taken."""
+    try:
+        txt = open(PROFILE).read()
+    except OSError:
+        return None
+    vals = dict(l.split(":", 1) for l in txt.splitlines() if l.startswith(("traffic_bytes", "kernel-source")))
+    if vals.get("kernel-source-sha256-16", "").split()[0:1] != [conv_source_hash()]:
+        return None
+    return int(vals["traffic_bytes_per_conv_launch"])
 
 
 def omp_threads():
@@ -78,6 +106,15 @@ def main():
     from paper_2003_01538_amd import flexserve as fsb
 
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": n, "launches": 5}))
+        return
     w = wl.workload(args.workload)
     B = w["batch"]
     imgs = list(wl.images_uniform(w["image_seed"], B, *w["in_hw"]))
@@ -134,7 +171,8 @@ def main():
         flops_per_launch = cv["flops"] / cv["launches"]
         achieved = flops_per_launch / (per_launch_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": counted_traffic(),
+                "algorithmic_bytes_per_launch": round(cv["bytes"] / cv["launches"]),
                 "kernel": "conv (implicit GEMM, all conv launches of a step)",
                 "avg_launch_us": round(per_launch_ms * 1e3, 2)}
         print(json.dumps({"profiled_ms_per_step": prof_s / args.steps * 1e3,
