@@ -161,8 +161,8 @@ def main():
         prof_s = time.perf_counter() - t0
         stats = fsb.fs_profile_read(ens.handle)
         if args.dump_launches:
-            per_step = info["launches_per_pass"]
-            recs = fsb.fs_profile_launches(ens.handle, max_out=per_step * args.steps)
+            recs = fsb.fs_profile_launches(ens.handle, max_out=info["launches_per_pass"] * args.steps)
+            per_step = len(recs) // args.steps  # records of one step (a split layer is one record)
             with open(args.dump_launches, "w") as f:
                 json.dump(recs[-per_step:], f, indent=0)
         fsb.fs_profile_enable(ens.handle, False)

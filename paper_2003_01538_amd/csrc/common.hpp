@@ -43,20 +43,26 @@ struct ConvArgs {
   int B, H, W, Cin, Ho, Wo, Cout;
   int kh, kw, stride, pad, relu;
   int K, Kp, M, Z;
+  int split = 1;            // K split over workgroups (LDS-DMA kernels only)
+  float* partial = nullptr; // split > 1: fp32 partial sums [split][Z][M][Cout]
 };
 struct ConvTile {
   int bm, bn, vec;   // block tile and A-load vector (elements)
   const char* name;
   int dma = 0;       // 0: register-staged gather kernel; >0: LDS-DMA kernel with this many stages
   int waves = 4;     // LDS-DMA kernel: waves per workgroup
+  int wgm = 2;       // LDS-DMA kernel: waves along M
 };
 int conv_num_tiles(Prec p);
 const ConvTile& conv_tile(Prec p, int t);
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a);
 bool conv_dma_ok(const ConvArgs& a);
-void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int stages, hipStream_t s);
-void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s);
+void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s);
+void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s);  // 1 or 2 launches (split-K reduce)
+int conv_split(Prec p, const ConvArgs& a, int num_cus);
+size_t conv_partial_floats(const ConvArgs& a);
+void launch_conv_splitk_reduce(const ConvArgs& a, hipStream_t s);
 constexpr int CONV_KPAD = 64;  // packed reduction length is a multiple of this
 
 // ------------------------------------------------------------------- pooling

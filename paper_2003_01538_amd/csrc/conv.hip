@@ -304,13 +304,16 @@ static const ConvTile kTilesBF16[] = {
     {128, 64, 4, "bf16_128x64_v4"},
     {64, 64, 4, "bf16_64x64_v4"},
     {256, 64, 8, "bf16_256x64_v8"},
-    {128, 128, 8, "bf16dma2_128x128_w4_v8", 2, 4},
-    {128, 64, 8, "bf16dma3_128x64_w4_v8", 3, 4},
-    {64, 128, 8, "bf16dma3_64x128_w4_v8", 3, 4},
-    {64, 64, 8, "bf16dma3_64x64_w4_v8", 3, 4},
-    {256, 128, 8, "bf16dma3_256x128_w8_v8", 3, 8},
-    {128, 256, 8, "bf16dma3_128x256_w8_v8", 3, 8},
-    {256, 64, 8, "bf16dma3_256x64_w8_v8", 3, 8},
+    {128, 128, 8, "bf16dma2_128x128_w4_v8", 2, 4, 2},
+    {128, 64, 8, "bf16dma3_128x64_w4_v8", 3, 4, 2},
+    {64, 128, 8, "bf16dma3_64x128_w4_v8", 3, 4, 2},
+    {64, 64, 8, "bf16dma3_64x64_w4_v8", 3, 4, 2},
+    {256, 128, 8, "bf16dma3_256x128_w8_v8", 3, 8, 4},
+    {128, 256, 8, "bf16dma3_128x256_w8_v8", 3, 8, 2},
+    {256, 64, 8, "bf16dma3_256x64_w8_v8", 3, 8, 4},
+    {128, 64, 8, "bf16dma2_128x64_w4_v8", 2, 4, 2},
+    {64, 128, 8, "bf16dma2_64x128_w4_v8", 2, 4, 2},
+    {256, 64, 8, "bf16dma2_256x64_w4m4_v8", 2, 4, 4},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -327,6 +330,7 @@ bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (t < 0 || t >= conv_num_tiles(p)) return false;
   const ConvTile& c = conv_tile(p, t);
   if (c.dma) return p == BF16 && conv_dma_ok(a);
+  if (a.split > 1) return false;  // only the LDS-DMA kernels split K
   return a.Cin % c.vec == 0 && a.Kp % CONV_KPAD == 0 && a.Cout % 8 == 0;
 }
 
@@ -362,7 +366,8 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
   if (p == BF16 && conv_tile(p, tile).dma) {
     const ConvTile& c = conv_tile(p, tile);
-    launch_conv_dma(a, c.bm, c.bn, c.waves, c.dma, s);
+    launch_conv_dma(a, c.bm, c.bn, c.waves, c.wgm, c.dma, s);
+    if (a.split > 1) launch_conv_splitk_reduce(a, s);
     return;
   }
   if (p == BF16) {

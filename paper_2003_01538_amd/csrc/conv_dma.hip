@@ -21,8 +21,9 @@
 //
 // Four or eight waves per workgroup, v_mfma_f32_32x32x16_bf16 (on gfx950
 // it sustains ~1.4x the rate of the 16x16x32 form), fp32 accumulators; the
-// epilogue (bias, residual, ReLU, bf16 store) goes through
-// LDS for 16-byte coalesced rows.  One launch covers the Z models of a group.
+// epilogue (bias, residual, ReLU, bf16 store) works on the accumulators in
+// registers, so LDS holds only the operand ring.  One launch covers the Z
+// models of a group.
 #include "common.hpp"
 #include "device.hpp"
 
@@ -58,8 +59,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   constexpr int AP = BM / (8 * NW), BP = BN / (8 * NW);  // DMA instructions per wave per tile
   constexpr int LPT = AP + BP;                             // vmcnt units per tile
   constexpr int STAGE = (BM + BN) * ROW;
-  constexpr int CS = BM * (BN + 4) * 4;
-  constexpr int SMEM = STAGES * STAGE > CS ? STAGES * STAGE : CS;
+  constexpr int SMEM = STAGES * STAGE;
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile");
   static_assert(AP * 8 * NW == BM && BP * 8 * NW == BN, "DMA blocks");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -70,8 +70,9 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
 
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.Cout + BN - 1) / BN;
   const int tiles = tiles_m * tiles_n;
-  const int id = xcd_remap(blockIdx.x, tiles * a.Z);
-  const int z = id / tiles, tile = id - z * tiles;
+  const int id = xcd_remap(blockIdx.x, tiles * a.Z * a.split);
+  const int tile = id % tiles, zs = id / tiles;
+  const int z = zs % a.Z, sp = zs / a.Z;
   const int mt = tile / tiles_n, ntile = tile - mt * tiles_n;
   const int m0 = mt * BM, n0 = ntile * BN;
 
@@ -170,14 +171,16 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ks][j], af[ks][i], acc[i][j], 0, 0, 0);
     }
   };
 
-  const int nk = a.Kp / BK;
+  // this workgroup's share of the K-tiles (all of them unless split-K)
+  const int nk_all = a.Kp / BK;
+  const int kb = sp * nk_all / a.split, nk = (sp + 1) * nk_all / a.split - kb;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s, s);
+    if (s < nk) issue(kb + s, s);
   for (int kt = 0; kt < nk; ++kt) {
     // tiles issued after kt that may stay in flight
     const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
@@ -191,52 +194,121 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
       else wait_vmcnt<0>();
     }
     __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    if (kt + STAGES - 1 < nk) issue(kb + kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     compute(kt % STAGES);
   }
-  __syncthreads();
 
-  // ---- epilogue: accumulators -> LDS -> coalesced rows.  32x32 result
-  // layout: lane l holds column (l & 31), rows 8g + 4(l >> 5) + r.
-  float* Cs = reinterpret_cast<float*>(smem);
-  constexpr int CSTR = BN + 4;
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          Cs[(wm * TM + i * 32 + g * 8 + fq * 4 + r) * CSTR + wn * TN + j * 32 + fr] = acc[i][j][g * 4 + r];
-  __syncthreads();
-
+  // ---- epilogue straight from the accumulators.  The MFMA computes
+  // D[n][m] (weights as the A operand), so lane l holds pixel m = l & 31 and
+  // channels 8g + 4q + r (q = l >> 5, r < 4) of each 32x32 block.  One
+  // permlane32 swap per register pair gives every lane 8 consecutive
+  // channels of one pixel: lanes 0-31 channels 8g.., lanes 32-63 channels
+  // 8(g+1).., for g = 0, 2.  Bias, residual, ReLU, bf16 rounding and a
+  // 16-byte store follow.
   const float* __restrict__ bias = a.bias + z * a.b_mstride;
   const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
   uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
-  constexpr int CPR = BN / 8;
-  for (int idx = tid; idx < BM * CPR; idx += NTH) {
-    const int row = idx / CPR, c8 = idx - row * CPR;
-    const int m = m0 + row, n = n0 + c8 * 8;
-    if (m >= a.M || n >= a.Cout) continue;
-    float v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = Cs[row * CSTR + c8 * 8 + e] + bias[n + e];
-    const int64_t o = (int64_t)m * a.Cout + n;
-    if (res) {
-      float r[8];
-      bf8_to_f8(*reinterpret_cast<const uint4*>(res + o), r);
+  for (int i = 0; i < FM; ++i) {
+    const int m = m0 + wm * TM + i * 32 + fr;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] += r[e];
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int gp = 0; gp < 4; gp += 2) {
+        float v[8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
+                                                           __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
+          v[r] = __uint_as_float(sw[0]);      // channels 8(gp+q) + r
+          v[4 + r] = __uint_as_float(sw[1]);  // channels 8(gp+q) + 4 + r
+        }
+        const int n = n0 + wn * TN + j * 32 + 8 * (gp + fq);
+        if (m >= a.M || n >= a.Cout) continue;
+        if (a.split > 1) {  // raw partial sums; the reduce kernel finishes
+          float4* pp = reinterpret_cast<float4*>(a.partial + (((int64_t)sp * a.Z + z) * a.M + m) * a.Cout + n);
+          pp[0] = make_float4(v[0], v[1], v[2], v[3]);
+          pp[1] = make_float4(v[4], v[5], v[6], v[7]);
+          continue;
+        }
+        const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+        const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+        v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+        v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+        const int64_t o = (int64_t)m * a.Cout + n;
+        if (res) {
+          float rr[8];
+          bf8_to_f8(*reinterpret_cast<const uint4*>(res + o), rr);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += rr[e];
+        }
+        if (a.relu)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+        *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
+      }
     }
-    if (a.relu)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
-    *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
   }
 }
 
+// Split-K completion: partial sums added in split order, then bias,
+// residual, ReLU and the bf16 store, 8 channels per thread.
+__global__ void __launch_bounds__(256) k_conv_splitk_reduce(ConvArgs a) {
+  const int cg = a.Cout / 8;
+  const int64_t total = (int64_t)a.Z * a.M * cg;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int c8 = (int)(i % cg);
+  const int64_t zm = i / cg;
+  const int z = (int)(zm / a.M), m = (int)(zm % a.M), n = c8 * 8;
+  float v[8];
+  const float4* p0 = reinterpret_cast<const float4*>(a.partial + ((int64_t)z * a.M + m) * a.Cout + n);
+  float4 q0 = p0[0], q1 = p0[1];
+  v[0] = q0.x; v[1] = q0.y; v[2] = q0.z; v[3] = q0.w; v[4] = q1.x; v[5] = q1.y; v[6] = q1.z; v[7] = q1.w;
+  for (int sp = 1; sp < a.split; ++sp) {
+    const float4* pp =
+        reinterpret_cast<const float4*>(a.partial + (((int64_t)sp * a.Z + z) * a.M + m) * a.Cout + n);
+    q0 = pp[0]; q1 = pp[1];
+    v[0] += q0.x; v[1] += q0.y; v[2] += q0.z; v[3] += q0.w;
+    v[4] += q1.x; v[5] += q1.y; v[6] += q1.z; v[7] += q1.w;
+  }
+  const float* bias = a.bias + z * a.b_mstride + n;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] += bias[e];
+  const int64_t o = (int64_t)m * a.Cout + n;
+  if (a.res) {
+    float r[8];
+    bf8_to_f8(*reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride + o), r);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] += r[e];
+  }
+  if (a.relu)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+  *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride + o) = f8_to_bf8(v);
+}
+
 }  // namespace
+
+void launch_conv_splitk_reduce(const ConvArgs& a, hipStream_t s) {
+  const int64_t total = (int64_t)a.Z * a.M * (a.Cout / 8);
+  hipLaunchKernelGGL(k_conv_splitk_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+}
+
+size_t conv_partial_floats(const ConvArgs& a) { return a.split > 1 ? (size_t)a.split * a.Z * a.M * a.Cout : 0; }
+
+// K split of a layer: a function of its shape only (never of the tile), so
+// every tile of the family still produces identical sums.  Split while the
+// layer has fewer than three 64x64 output tiles per CU, keeping >= 8 K-tiles
+// per split.
+int conv_split(Prec p, const ConvArgs& a, int num_cus) {
+  if (p != BF16 || !conv_dma_ok(a)) return 1;
+  const int64_t units = (int64_t)((a.M + 63) / 64) * ((a.Cout + 63) / 64) * a.Z;
+  const int nk = a.Kp / BK;
+  int split = 1;
+  while (units * split < 3 * num_cus && split < 4 && nk / (split * 2) >= 8) split *= 2;
+  return split;
+}
 
 // Every 64-wide K-tile must lie in one filter row and cover whole pixels.
 bool conv_dma_ok(const ConvArgs& a) {
@@ -244,10 +316,10 @@ bool conv_dma_ok(const ConvArgs& a) {
   return tiles_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0;
 }
 
-void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int stages, hipStream_t s) {
-  const int tiles = ((a.M + bm - 1) / bm) * ((a.Cout + bn - 1) / bn) * a.Z;
+void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s) {
+  const int tiles = ((a.M + bm - 1) / bm) * ((a.Cout + bn - 1) / bn) * a.Z * a.split;
 #define FS_DMA(BMv, BNv, WMv, WNv, Sv)                                                                   \
-  if (bm == BMv && bn == BNv && waves == WMv * WNv && stages == Sv) {                                    \
+  if (bm == BMv && bn == BNv && waves == WMv * WNv && stages == Sv && wgm == WMv) {                                    \
     hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
     return;                                                                                              \
   }
@@ -258,6 +330,9 @@ void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int stages, h
   FS_DMA(256, 128, 4, 2, 3)
   FS_DMA(128, 256, 2, 4, 3)
   FS_DMA(256, 64, 4, 2, 3)
+  FS_DMA(128, 64, 2, 2, 2)
+  FS_DMA(64, 128, 2, 2, 2)
+  FS_DMA(256, 64, 4, 1, 2)
 #undef FS_DMA
 }
 

@@ -157,6 +157,7 @@ struct fs_ensemble {
   DevBuf input_s2d; // [max_batch][out_h/2][out_w/2][16] bf16
   bool need_plain = false, need_s2d = false;
   DevBuf partial;   // fc split-K scratch
+  DevBuf conv_partial;  // conv split-K scratch (grown when a batch bucket is first planned)
   DevBuf logits;    // [N][max_batch][C] fp32
   // host-path staging
   DevBuf d_pixels, d_desc, d_probs, d_mean, d_vote, d_top1;
@@ -619,6 +620,8 @@ ConvArgs conv_args(fs_ensemble* e, Group& g, const LayerPlan& P, int B, void* y,
   a.Ho = P.out.H; a.Wo = P.out.W; a.Cout = P.out.C;
   a.kh = P.kh; a.kw = P.kw; a.stride = P.stride; a.pad = P.pad; a.relu = P.relu;
   a.K = P.K; a.Kp = P.Kp; a.M = B * P.out.H * P.out.W; a.Z = g.Z;
+  a.split = conv_split(e->prec, a, e->num_cus);
+  a.partial = static_cast<float*>(e->conv_partial.p);
   return a;
 }
 
@@ -651,6 +654,13 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
       LayerPlan& P = g.layers[li];
       if (P.op != FS_OP_CONV) continue;
       ConvArgs a = conv_args(e, g, P, bucket, slot_ptr(g, P.out_slot), (int64_t)g.slot_elems[P.out_slot] * e->max_batch);
+      const size_t need = conv_partial_floats(a) * 4;
+      if (need > e->conv_partial.bytes) {  // split-K scratch for this bucket
+        HIPCHK(hipStreamSynchronize(s));
+        e->conv_partial.alloc(round_up(need, 256));
+        e->workspace_bytes += (int64_t)e->conv_partial.bytes;
+        a.partial = static_cast<float*>(e->conv_partial.p);
+      }
       bool any_dma = false;
       for (int t = 0; t < conv_num_tiles(e->prec); ++t)
         if (conv_tile_ok(e->prec, t, a) && conv_tile(e->prec, t).dma) any_dma = true;
@@ -736,7 +746,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           const double in_b = (double)B * P.in.H * P.in.W * P.in_c_real * (P.s2d ? 4 : 1) * esz *
                               (P.in_slot == SLOT_INPUT ? 1 : g.Z);
           const double bytes = in_b + ((double)a.Cout * kreal * esz + (double)a.M * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
-          launch(K_CONV, flops, bytes, 1, [&] { launch_conv(a, p, tile, s); });
+          launch(K_CONV, flops, bytes, a.split > 1 ? 2 : 1, [&] { launch_conv(a, p, tile, s); });
           break;
         }
         case FS_OP_MAXPOOL:
@@ -793,8 +803,14 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
 int launches_per_pass(fs_ensemble* e) {
   int n = 1 + (e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0);  // preprocess + softmax/combine
   for (Group& g : e->groups)
-    for (LayerPlan& P : g.layers)
-      n += P.op == FS_OP_FC ? fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus)) : 1;
+    for (LayerPlan& P : g.layers) {
+      if (P.op == FS_OP_FC)
+        n += fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus));
+      else if (P.op == FS_OP_CONV)
+        n += conv_args(e, g, P, e->max_batch, nullptr, 0).split > 1 ? 2 : 1;
+      else
+        n += 1;
+    }
   return n;
 }
 
@@ -1203,6 +1219,10 @@ fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t
     int tl = tile;
     if (tl < 0) tl = conv_pick_tile(p, a, num_cus_of(device));
     if (!conv_tile_ok(p, tl, a)) fail(FS_ERR_UNSUPPORTED, "tile " + std::to_string(tile) + " does not fit this conv");
+    if (conv_tile(p, tl).dma) {  // the ensemble's split rule, so split-K is exercised too
+      a.split = conv_split(p, a, num_cus_of(device));
+      if (a.split > 1) a.partial = static_cast<float*>(t.alloc(conv_partial_floats(a) * 4));
+    }
     launch_conv(a, p, tl, nullptr);
     HIPCHK(hipGetLastError());
     HIPCHK(hipDeviceSynchronize());
@@ -1364,6 +1384,10 @@ fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Co
     a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = Z;
     int tl = tile < 0 ? conv_pick_tile(p, a, num_cus_of(device)) : tile;
     if (!conv_tile_ok(p, tl, a)) fail(FS_ERR_UNSUPPORTED, "tile does not fit this conv");
+    if (conv_tile(p, tl).dma) {
+      a.split = conv_split(p, a, num_cus_of(device));
+      if (a.split > 1) a.partial = static_cast<float*>(t.alloc(conv_partial_floats(a) * 4));
+    }
     if (tile_used) *tile_used = tl;
     hipStream_t s = nullptr;
     for (int i = 0; i < 3; ++i) launch_conv(a, p, tl, s);
