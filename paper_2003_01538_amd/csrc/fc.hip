@@ -1,12 +1,13 @@
 // Fully connected layer y[b][n] = relu?(bias[n] + sum_k x[b][k] * w[n][k]) on
 // the matrix cores.  At serving batch sizes the layer streams its weights
 // once (arithmetic intensity = B FLOP per weight byte), so the kernel is
-// built to keep HBM busy rather than to tile for reuse: every wave owns 16
-// output features, reads its weight rows straight from global memory with
-// 16-byte loads (no LDS; each weight is used by exactly one wave) and
-// multiplies them with 16*FB batch columns per MFMA step.  Large K is split
-// over grid.z (split-K) into an fp32 scratch that a second small kernel sums
-// in a fixed order, so results do not depend on scheduling.
+// built to keep HBM busy rather than to tile for reuse: a workgroup owns 16
+// output features, its waves read weight rows straight from global memory
+// with 16-byte loads (no LDS staging; each weight is used by exactly one
+// wave) and multiply them with 16*FB batch columns per MFMA step.  Large K
+// is also split over grid.z (split-K) into an fp32 scratch that a second
+// small kernel sums in a fixed order, so results do not depend on
+// scheduling.
 //
 // MFMA operands: A = 16 weight rows (features), B = 16 batch rows, so each
 // lane's accumulator holds 4 consecutive features of one image.
@@ -23,12 +24,17 @@ template <> struct FcT<F32> { using T = float; static constexpr int KSTEP = 4; }
 
 constexpr int FC_UNROLL = 4;
 
+// One workgroup = 16 output features x 16*FB images; its 4 waves take
+// interleaved quarters of the K steps and their accumulators are added in
+// wave order through LDS.  grid.z = split * Z (split-K over workgroups for
+// very long K, finished by k_fc_reduce).
 template <int P, int FB>
 __global__ void __launch_bounds__(256) k_fc(FcArgs a) {
   using T = typename FcT<P>::T;
   constexpr int KSTEP = FcT<P>::KSTEP;
+  __shared__ floatx4 red[3][FB][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.x * 64 + wave * 16;
+  const int n0 = blockIdx.x * 16;
   const int b0 = blockIdx.y * 16 * FB;
   const int model = blockIdx.z / a.split, sp = blockIdx.z - model * a.split;
   const T* __restrict__ x = reinterpret_cast<const T*>(a.x) + model * a.x_mstride;
@@ -58,18 +64,18 @@ __global__ void __launch_bounds__(256) k_fc(FcArgs a) {
 #pragma unroll
   for (int f = 0; f < FB; ++f) acc[f] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k = kb; k < ke; k += KSTEP * FC_UNROLL) {
+  // wave w takes steps w, w+4, ... in groups of FC_UNROLL
+  for (int k = kb + wave * KSTEP; k < ke; k += 4 * KSTEP * FC_UNROLL) {
     if constexpr (P == BF16) {
       uint4 wa[FC_UNROLL], xb[FC_UNROLL][FB];
 #pragma unroll
       for (int u = 0; u < FC_UNROLL; ++u) {
-        const int kk = k + u * KSTEP + koff;
-        const bool kin = kk + LE <= ke;
-        wa[u] = (kin && n_ok) ? *reinterpret_cast<const uint4*>(wrow + k + u * KSTEP) : uint4{0, 0, 0, 0};
+        const int ku = k + u * 4 * KSTEP;
+        const bool kin = ku + koff + LE <= ke;
+        wa[u] = (kin && n_ok) ? *reinterpret_cast<const uint4*>(wrow + ku) : uint4{0, 0, 0, 0};
 #pragma unroll
         for (int f = 0; f < FB; ++f)
-          xb[u][f] = (kin && b_ok[f]) ? *reinterpret_cast<const uint4*>(xrow[f] + k + u * KSTEP)
-                                      : uint4{0, 0, 0, 0};
+          xb[u][f] = (kin && b_ok[f]) ? *reinterpret_cast<const uint4*>(xrow[f] + ku) : uint4{0, 0, 0, 0};
       }
 #pragma unroll
       for (int u = 0; u < FC_UNROLL; ++u)
@@ -82,11 +88,11 @@ __global__ void __launch_bounds__(256) k_fc(FcArgs a) {
       float wa[FC_UNROLL], xb[FC_UNROLL][FB];
 #pragma unroll
       for (int u = 0; u < FC_UNROLL; ++u) {
-        const int kk = k + u * KSTEP + koff;
-        const bool kin = kk < ke;
-        wa[u] = (kin && n_ok) ? wrow[k + u * KSTEP] : 0.f;
+        const int ku = k + u * 4 * KSTEP;
+        const bool kin = ku + koff < ke;
+        wa[u] = (kin && n_ok) ? wrow[ku] : 0.f;
 #pragma unroll
-        for (int f = 0; f < FB; ++f) xb[u][f] = (kin && b_ok[f]) ? xrow[f][k + u * KSTEP] : 0.f;
+        for (int f = 0; f < FB; ++f) xb[u][f] = (kin && b_ok[f]) ? xrow[f][ku] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < FC_UNROLL; ++u)
@@ -95,6 +101,17 @@ __global__ void __launch_bounds__(256) k_fc(FcArgs a) {
           acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[u], xb[u][f], acc[f], 0, 0, 0);
     }
   }
+
+  // waves 1..3 hand their sums to wave 0, which adds them in wave order
+  if (wave > 0)
+#pragma unroll
+    for (int f = 0; f < FB; ++f) red[wave - 1][f][lane] = acc[f];
+  __syncthreads();
+  if (wave > 0) return;
+#pragma unroll
+  for (int f = 0; f < FB; ++f)
+#pragma unroll
+    for (int q = 0; q < 3; ++q) acc[f] += red[q][f][lane];
 
   // acc[f][r] = y[b = b0 + 16f + (lane & 15)][n = n0 + 4 (lane >> 4) + r]
   const float* bias = a.bias + model * a.b_mstride;
@@ -145,9 +162,10 @@ static int fc_fb(int B) { return B > 32 ? 4 : (B > 16 ? 2 : 1); }
 
 int fc_pick_split(Prec p, int B, int K, int N, int Z, int num_cus) {
   const int fb = fc_fb(B);
-  const int wgs = ((N + 63) / 64) * ((B + 16 * fb - 1) / (16 * fb)) * Z;
+  const int wgs = ((N + 15) / 16) * ((B + 16 * fb - 1) / (16 * fb)) * Z;
   const int kstep = p == BF16 ? 32 : 4;
-  const int max_split = std::max(1, K / (kstep * FC_UNROLL * 4));  // >= 4 unrolled steps per split
+  // each split keeps >= 4 unrolled step groups for every one of the 4 waves
+  const int max_split = std::max(1, K / (kstep * FC_UNROLL * 4 * 4));
   int split = (2 * num_cus + wgs - 1) / wgs;
   return std::max(1, std::min(split, std::min(max_split, 32)));
 }
@@ -160,7 +178,7 @@ int fc_launches(int split) { return split > 1 ? 2 : 1; }
 
 template <int P, int FB>
 static void launch_fc_t(const FcArgs& a, hipStream_t s) {
-  dim3 grid((a.N + 63) / 64, (a.B + 16 * FB - 1) / (16 * FB), a.split * a.Z);
+  dim3 grid((a.N + 15) / 16, (a.B + 16 * FB - 1) / (16 * FB), a.split * a.Z);
   hipLaunchKernelGGL((k_fc<P, FB>), grid, dim3(256), 0, s, a);
 }
 

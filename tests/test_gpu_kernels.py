@@ -67,9 +67,13 @@ def test_preprocess_parity(gpu_lib, prec, case):
 
 
 def test_preprocess_space_to_depth_layout(gpu_lib):
-    imgs = wl.images_ragged(4000, 3) + [wl.images_uniform(5, 1, 224, 224)[0]]
+    rng = np.random.default_rng(4001)
+    # ragged sizes, a square image, a strided view and a very wide image
+    big = rng.integers(0, 256, (300, 420, 3), dtype=np.uint8)
+    imgs = (wl.images_ragged(4000, 3) + [wl.images_uniform(5, 1, 224, 224)[0]]
+            + [big[7:290, 11:400], rng.integers(0, 256, (37, 1500, 3), dtype=np.uint8)])
     g = fsb.fs_test_preprocess(imgs, 224, 224, MEAN, STD, BF16, layout=1)
-    assert g.shape == (4, 112, 112, 16) and np.all(g[..., 12:] == 0)
+    assert g.shape == (len(imgs), 112, 112, 16) and np.all(g[..., 12:] == 0)
     for i, im in enumerate(imgs):
         o = oracle.preprocess(im, 224, 224, MEAN, STD, "bf16")
         # channel (sy*2 + sx)*3 + c of block (Y, X) is pixel (2Y+sy, 2X+sx), channel c
@@ -151,7 +155,8 @@ def test_conv_repeat_is_bit_identical(gpu_lib):
 
 # -------------------------------------------------------------------- pooling
 @pytest.mark.parametrize("prec", [BF16, F32])
-@pytest.mark.parametrize("k,s,p,hw", [(3, 2, 1, (17, 16)), (2, 2, 0, (16, 14)), (3, 2, 1, (112, 112))])
+@pytest.mark.parametrize("k,s,p,hw", [(3, 2, 1, (17, 16)), (2, 2, 0, (16, 14)), (3, 2, 1, (112, 112)),
+                                      (3, 1, 1, (9, 5))])
 def test_maxpool_bit_exact(gpu_lib, prec, k, s, p, hw):
     rng = np.random.default_rng(k * 10 + hw[0])
     x = rng.standard_normal((2,) + hw + (64,)).astype(np.float32)
