@@ -11,8 +11,12 @@
 // LDS[M0 + 16 j] without touching VGPRs; offsets past the buffer read as
 // zero, which supplies the convolution's zero padding and the rows/columns
 // past M and N.  A wave instruction fills 8 tile rows (1 KB).  Rows are
-// stored unpadded with their eight 16-byte chunks XOR-swizzled by (row & 7),
-// so the 16 rows an MFMA operand read touches fall on distinct banks.
+// stored unpadded with their eight 16-byte chunks XOR-swizzled by
+// swz(row) = (row & 7) ^ ((row >> 3) & 1): an operand read serves 16 lanes
+// (16 rows x 16 bytes) per cycle from 64 four-byte banks, and consecutive
+// rows alternate between the two 128-byte bank halves, so the 16 rows need
+// distinct chunks within each parity class, which (row & 7) alone does not
+// give for rows r and r + 8.
 //
 // Pipeline: STAGES LDS buffers.  Iteration k waits (vmcnt) for its own
 // wave's loads of tile k, meets the other waves at one barrier (after which
@@ -36,6 +40,8 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int BK = 64;          // bf16 elements per K-tile row (128 bytes)
 constexpr int ROW = 128;        // LDS bytes per tile row
 constexpr uint32_t OOB = 0x80000000u;
+
+__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -62,6 +68,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   constexpr int SMEM = STAGES * STAGE;
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile");
   static_assert(AP * 8 * NW == BM && BP * 8 * NW == BN, "DMA blocks");
+  static_assert(NW % 2 == 0, "the swizzle of a DMA block's rows depends on the wave only");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -81,10 +88,11 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   const __amdgpu_buffer_rsrc_t rw = rsrc(reinterpret_cast<const uint16_t*>(a.w) + z * a.w_mstride,
                                          (uint32_t)((int64_t)a.Cout * a.Kp * 2));
 
-  // lane j of a DMA instruction writes LDS row (j >> 3) of its 8-row block,
-  // physical chunk (j & 7), which holds logical chunk (j & 7) ^ (j >> 3)
+  // lane j of a DMA instruction writes LDS row (j >> 3) of its 8-row block
+  // (block i * NW + wave, so row bit 3 is the wave's parity), physical chunk
+  // (j & 7), which holds logical chunk (j & 7) ^ swz(row)
   const int lr = lane >> 3;
-  const int lc = (lane & 7) ^ lr;
+  const int lc = (lane & 7) ^ lr ^ (wave & 1);
   // when Cin < 64 a 64-wide K-tile spans 64 / Cin consecutive pixels of one
   // filter row: this lane's 8 channels belong to pixel kx + dx
   const int dx = (lc * 8) / a.Cin;
@@ -157,12 +165,12 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int r = wm * TM + i * 32 + fr;
-          af[ks][i] = *reinterpret_cast<const bf16x8*>(As + r * ROW + ((c ^ (r & 7)) << 4));
+          af[ks][i] = *reinterpret_cast<const bf16x8*>(As + r * ROW + ((c ^ swz(r)) << 4));
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int r = wn * TN + j * 32 + fr;
-          bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + r * ROW + ((c ^ (r & 7)) << 4));
+          bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + r * ROW + ((c ^ swz(r)) << 4));
         }
       }
 #pragma unroll
