@@ -53,6 +53,9 @@ struct ConvTile {
   int waves = 4;     // LDS-DMA kernel: waves per workgroup
   int wgm = 2;       // LDS-DMA kernel: waves along M
 };
+// Every LDS-DMA tile shares one MFMA step and K order, so all of them
+// produce bit-identical sums.
+inline bool conv_tile_direct(const ConvTile& c) { return c.dma > 0; }
 int conv_num_tiles(Prec p);
 const ConvTile& conv_tile(Prec p, int t);
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);

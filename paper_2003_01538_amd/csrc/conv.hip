@@ -309,7 +309,6 @@ static const ConvTile kTilesBF16[] = {
     {64, 128, 8, "bf16dma3_64x128_w4_v8", 3, 4, 2},
     {64, 64, 8, "bf16dma3_64x64_w4_v8", 3, 4, 2},
     {256, 128, 8, "bf16dma3_256x128_w8_v8", 3, 8, 4},
-    {128, 256, 8, "bf16dma3_128x256_w8_v8", 3, 8, 2},
     {256, 64, 8, "bf16dma3_256x64_w8_v8", 3, 8, 4},
     {128, 64, 8, "bf16dma2_128x64_w4_v8", 2, 4, 2},
     {64, 128, 8, "bf16dma2_64x128_w4_v8", 2, 4, 2},
@@ -329,7 +328,7 @@ const ConvTile& conv_tile(Prec p, int t) { return p == BF16 ? kTilesBF16[t] : kT
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (t < 0 || t >= conv_num_tiles(p)) return false;
   const ConvTile& c = conv_tile(p, t);
-  if (c.dma) return p == BF16 && conv_dma_ok(a);
+  if (conv_tile_direct(c)) return p == BF16 && conv_dma_ok(a);
   if (a.split > 1) return false;  // only the LDS-DMA kernels split K
   return a.Cin % c.vec == 0 && a.Kp % CONV_KPAD == 0 && a.Cout % 8 == 0;
 }
@@ -348,7 +347,7 @@ int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus) {
     const double fill = wgs >= 2.0 * num_cus ? 1.0 : wgs / (2.0 * num_cus);
     const double reuse = (double)c.bm * c.bn / (c.bm + c.bn) / 64.0;  // 1.0 for 128x128
     const double score = useful * (0.35 + 0.65 * fill) * (0.6 + 0.4 * reuse) *
-                         (c.vec == 8 || p == F32 ? 1.0 : 0.9) * (c.dma ? 1.5 : 1.0);
+                         (c.vec == 8 || p == F32 ? 1.0 : 0.9) * (conv_tile_direct(c) ? 1.5 : 1.0);
     if (score > best_score) { best_score = score; best = t; }
   }
   return best;
@@ -364,7 +363,7 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
 }
 
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
-  if (p == BF16 && conv_tile(p, tile).dma) {
+  if (p == BF16 && conv_tile_direct(conv_tile(p, tile))) {
     const ConvTile& c = conv_tile(p, tile);
     launch_conv_dma(a, c.bm, c.bn, c.waves, c.wgm, c.dma, s);
     if (a.split > 1) launch_conv_splitk_reduce(a, s);

@@ -54,6 +54,123 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Wait until at most `ahead` K-tiles (LPT load instructions each) of this
+// wave are still in flight; `ahead` <= A (vmcnt takes an immediate).
+template <int A, int LPT>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if constexpr (A <= 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= A) wait_vmcnt<A * LPT>();
+    else wait_tiles<A - 1, LPT>(ahead);
+  }
+}
+
+// MFMAs of one 64-wide K-tile for a wave's TM x TN sub-tile (FM x FN blocks of
+// 32x32).  32x32x16 operands: lane l supplies row (l & 31), k-group (l >> 5)
+// of 8; the weights are the A operand, so block (i, j) accumulates D[n][m].
+template <int FM, int FN>
+__device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int row_a, int row_b, int lane,
+                                          floatx16 (&acc)[FM][FN]) {
+  const int fr = lane & 31, fq = lane >> 5;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh) {  // two halves of the 64-wide K-tile
+    bf16x8 af[2][FM], bfr[2][FN];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = (kh * 2 + ks) * 2 + fq;  // logical 16-byte chunk
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int r = row_a + i * 32 + fr;
+        af[ks][i] = *reinterpret_cast<const bf16x8*>(As + r * ROW + ((c ^ swz(r)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int r = row_b + j * 32 + fr;
+        bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + r * ROW + ((c ^ swz(r)) << 4));
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ks][j], af[ks][i], acc[i][j], 0, 0, 0);
+  }
+}
+
+// Epilogue straight from the accumulators.  The MFMA computes D[n][m]
+// (weights as the A operand), so lane l holds pixel m = l & 31 and channels
+// 8g + 4q + r (q = l >> 5, r < 4) of each 32x32 block.  One permlane32 swap
+// per register pair gives every lane 8 consecutive channels of one pixel:
+// lanes 0-31 channels 8g.., lanes 32-63 channels 8(g+1).., for g = 0, 2.
+// Bias, residual, ReLU, bf16 rounding and a 16-byte store follow; with a K
+// split the raw fp32 sums go to the partial buffer instead.
+template <int FM, int FN>
+__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)[FM][FN], int mrow, int ncol,
+                                              int z, int sp, int lane) {
+  const int fr = lane & 31, fq = lane >> 5;
+  const float* __restrict__ bias = a.bias + z * a.b_mstride;
+  const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
+  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int m = mrow + i * 32 + fr;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int gp = 0; gp < 4; gp += 2) {
+        float v[8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
+                                                           __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
+          v[r] = __uint_as_float(sw[0]);      // channels 8(gp+q) + r
+          v[4 + r] = __uint_as_float(sw[1]);  // channels 8(gp+q) + 4 + r
+        }
+        const int n = ncol + j * 32 + 8 * (gp + fq);
+        if (m >= a.M || n >= a.Cout) continue;
+        if (a.split > 1) {  // raw partial sums; the reduce kernel finishes
+          float4* pp = reinterpret_cast<float4*>(a.partial + (((int64_t)sp * a.Z + z) * a.M + m) * a.Cout + n);
+          pp[0] = make_float4(v[0], v[1], v[2], v[3]);
+          pp[1] = make_float4(v[4], v[5], v[6], v[7]);
+          continue;
+        }
+        const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+        const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+        v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+        v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+        const int64_t o = (int64_t)m * a.Cout + n;
+        if (res) {
+          float rr[8];
+          bf8_to_f8(*reinterpret_cast<const uint4*>(res + o), rr);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += rr[e];
+        }
+        if (a.relu)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+        *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
+      }
+    }
+  }
+}
+
+// Tile of workgroup `bid` among tiles * Z * split, XCD-contiguous.
+struct TileCoord {
+  int m0, n0, z, sp;
+};
+template <int BM, int BN>
+__device__ __forceinline__ TileCoord tile_coord(const ConvArgs& a, int bid) {
+  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.Cout + BN - 1) / BN;
+  const int tiles = tiles_m * tiles_n;
+  const int id = xcd_remap(bid, tiles * a.Z * a.split);
+  const int tile = id % tiles, zs = id / tiles;
+  const int mt = tile / tiles_n, nt = tile - mt * tiles_n;
+  return TileCoord{mt * BM, nt * BN, zs % a.Z, zs / a.Z};
+}
+
 // BM x BN block tile, WGM x WGN waves (wave tile BM/WGM x BN/WGN, multiples
 // of 32), v_mfma_f32_32x32x16_bf16.
 template <int BM, int BN, int WGM, int WGN, int STAGES>
@@ -75,13 +192,8 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
 
-  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.Cout + BN - 1) / BN;
-  const int tiles = tiles_m * tiles_n;
-  const int id = xcd_remap(blockIdx.x, tiles * a.Z * a.split);
-  const int tile = id % tiles, zs = id / tiles;
-  const int z = zs % a.Z, sp = zs / a.Z;
-  const int mt = tile / tiles_n, ntile = tile - mt * tiles_n;
-  const int m0 = mt * BM, n0 = ntile * BN;
+  const TileCoord tc = tile_coord<BM, BN>(a, blockIdx.x);
+  const int m0 = tc.m0, n0 = tc.n0, z = tc.z, sp = tc.sp;
 
   const __amdgpu_buffer_rsrc_t rx = rsrc(reinterpret_cast<const uint16_t*>(a.x) + z * a.x_mstride,
                                          (uint32_t)((int64_t)a.B * a.H * a.W * a.Cin * 2));
@@ -151,36 +263,9 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  // 32x32x16 operands: lane l supplies row (l & 31), k-group (l >> 5) of 8
-  const int fr = lane & 31, fq = lane >> 5;
   auto compute = [&](int stage) {
     const char* As = smem + stage * STAGE;
-    const char* Bs = As + BM * ROW;
-#pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {  // two halves of the 64-wide K-tile
-      bf16x8 af[2][FM], bfr[2][FN];
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int c = (kh * 2 + ks) * 2 + fq;  // logical 16-byte chunk
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          const int r = wm * TM + i * 32 + fr;
-          af[ks][i] = *reinterpret_cast<const bf16x8*>(As + r * ROW + ((c ^ swz(r)) << 4));
-        }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int r = wn * TN + j * 32 + fr;
-          bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + r * ROW + ((c ^ swz(r)) << 4));
-        }
-      }
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ks][j], af[ks][i], acc[i][j], 0, 0, 0);
-    }
+    mma_ktile<FM, FN>(As, As + BM * ROW, wm * TM, wn * TN, lane, acc);
   };
 
   // this workgroup's share of the K-tiles (all of them unless split-K)
@@ -192,71 +277,13 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   for (int kt = 0; kt < nk; ++kt) {
     // tiles issued after kt that may stay in flight
     const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
-    if constexpr (STAGES == 2) {
-      wait_vmcnt<0>();
-    } else if constexpr (STAGES == 3) {
-      if (ahead >= 1) wait_vmcnt<LPT>(); else wait_vmcnt<0>();
-    } else {
-      if (ahead >= 2) wait_vmcnt<2 * LPT>();
-      else if (ahead == 1) wait_vmcnt<LPT>();
-      else wait_vmcnt<0>();
-    }
+    wait_tiles<STAGES - 2, LPT>(ahead);
     __builtin_amdgcn_s_barrier();
     if (kt + STAGES - 1 < nk) issue(kb + kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     compute(kt % STAGES);
   }
 
-  // ---- epilogue straight from the accumulators.  The MFMA computes
-  // D[n][m] (weights as the A operand), so lane l holds pixel m = l & 31 and
-  // channels 8g + 4q + r (q = l >> 5, r < 4) of each 32x32 block.  One
-  // permlane32 swap per register pair gives every lane 8 consecutive
-  // channels of one pixel: lanes 0-31 channels 8g.., lanes 32-63 channels
-  // 8(g+1).., for g = 0, 2.  Bias, residual, ReLU, bf16 rounding and a
-  // 16-byte store follow.
-  const float* __restrict__ bias = a.bias + z * a.b_mstride;
-  const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
-  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int m = m0 + wm * TM + i * 32 + fr;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-#pragma unroll
-      for (int gp = 0; gp < 4; gp += 2) {
-        float v[8];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
-                                                           __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
-          v[r] = __uint_as_float(sw[0]);      // channels 8(gp+q) + r
-          v[4 + r] = __uint_as_float(sw[1]);  // channels 8(gp+q) + 4 + r
-        }
-        const int n = n0 + wn * TN + j * 32 + 8 * (gp + fq);
-        if (m >= a.M || n >= a.Cout) continue;
-        if (a.split > 1) {  // raw partial sums; the reduce kernel finishes
-          float4* pp = reinterpret_cast<float4*>(a.partial + (((int64_t)sp * a.Z + z) * a.M + m) * a.Cout + n);
-          pp[0] = make_float4(v[0], v[1], v[2], v[3]);
-          pp[1] = make_float4(v[4], v[5], v[6], v[7]);
-          continue;
-        }
-        const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
-        const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
-        v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
-        v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
-        const int64_t o = (int64_t)m * a.Cout + n;
-        if (res) {
-          float rr[8];
-          bf8_to_f8(*reinterpret_cast<const uint4*>(res + o), rr);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] += rr[e];
-        }
-        if (a.relu)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
-        *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
-      }
-    }
-  }
+  conv_epilogue<FM, FN>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane);
 }
 
 // Split-K completion: partial sums added in split order, then bias,
@@ -336,7 +363,6 @@ void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int 
   FS_DMA(64, 128, 2, 2, 3)
   FS_DMA(64, 64, 2, 2, 3)
   FS_DMA(256, 128, 4, 2, 3)
-  FS_DMA(128, 256, 2, 4, 3)
   FS_DMA(256, 64, 4, 2, 3)
   FS_DMA(128, 64, 2, 2, 2)
   FS_DMA(64, 128, 2, 2, 2)
