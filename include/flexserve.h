@@ -200,6 +200,17 @@ fs_status fs_test_conv(const float *in, int32_t B, int32_t H, int32_t W, int32_t
                        int32_t kh, int32_t kw, int32_t stride, int32_t pad, int32_t relu,
                        int32_t precision, int32_t tile, float *out, int32_t device);
 
+/* The ResNet stem as the ensemble runs it in bf16: conv 7x7 / stride 2 /
+ * pad 3 from 3 channels to 64 (in its space-to-depth form), + bias, ReLU,
+ * bf16 rounding, then max pool 3x3 / stride 2 / pad 1 (He et al., the
+ * ResNet stem; the paper's models are such CNNs, Sec. 2.2), in one kernel.
+ * in [B][H][W][3] (H, W even), w [64][7][7][3], bias [64] or NULL,
+ * out [B][Hp][Wp][64] with Ho = H/2, Hp = (Ho - 1)/2 + 1 (likewise W).
+ * FS_ERR_UNSUPPORTED when the shape is not one the fused kernel takes
+ * (conv output wider than 112). */
+fs_status fs_test_stem_pool(const float *in, int32_t B, int32_t H, int32_t W, const float *w,
+                            const float *bias, float *out, int32_t device);
+
 fs_status fs_test_maxpool(const float *in, int32_t B, int32_t H, int32_t W, int32_t C,
                           int32_t k, int32_t stride, int32_t pad, int32_t precision,
                           float *out, int32_t device);

@@ -52,16 +52,28 @@ struct ConvTile {
   int dma = 0;       // 0: register-staged gather kernel; >0: LDS-DMA kernel with this many stages
   int waves = 4;     // LDS-DMA kernel: waves per workgroup
   int wgm = 2;       // LDS-DMA kernel: waves along M
+  int halo = 0;      // 1: direct 3x3 kernel with the input halo in LDS,
+  int th = 0, tw = 0;  //    tiles of th output rows x tw (= output width) columns
 };
 // Every LDS-DMA tile shares one MFMA step and K order, so all of them
 // produce bit-identical sums.
 inline bool conv_tile_direct(const ConvTile& c) { return c.dma > 0; }
+// Kernel family of a tile: 2 halo, 1 LDS-DMA implicit GEMM, 0 register-staged
+// implicit GEMM.  A layer always runs in the highest family that fits it, and
+// tiles are only ever compared within one family.
+inline int conv_tile_family(const ConvTile& c) { return c.halo ? 2 : (c.dma > 0 ? 1 : 0); }
 int conv_num_tiles(Prec p);
 const ConvTile& conv_tile(Prec p, int t);
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a);
 bool conv_dma_ok(const ConvArgs& a);
 void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s);
+bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn);
+// Space-to-depth ResNet stem (4x4/1/p2 on 16 channels, 64 outputs, ReLU)
+// fused with the following 3x3/2/p1 max pool; y receives the pooled tensor.
+bool conv_stem_pool_ok(const ConvArgs& a);
+void launch_conv_stem_pool(const ConvArgs& a, hipStream_t s);
+void launch_conv_halo(const ConvArgs& a, int th, int tw, int bn, hipStream_t s);
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s);  // 1 or 2 launches (split-K reduce)
 int conv_split(Prec p, const ConvArgs& a, int num_cus);
 size_t conv_partial_floats(const ConvArgs& a);

@@ -20,6 +20,8 @@
 #include "common.hpp"
 #include "device.hpp"
 
+#include <algorithm>
+
 namespace fs {
 
 template <int P> struct PT;
@@ -313,6 +315,7 @@ static const ConvTile kTilesBF16[] = {
     {128, 64, 8, "bf16dma2_128x64_w4_v8", 2, 4, 2},
     {64, 128, 8, "bf16dma2_64x128_w4_v8", 2, 4, 2},
     {256, 64, 8, "bf16dma2_256x64_w4m4_v8", 2, 4, 4},
+    {224, 64, 8, "bf16halo_4x56_n64_v8", 0, 7, 7, 1, 4, 56},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -328,6 +331,7 @@ const ConvTile& conv_tile(Prec p, int t) { return p == BF16 ? kTilesBF16[t] : kT
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (t < 0 || t >= conv_num_tiles(p)) return false;
   const ConvTile& c = conv_tile(p, t);
+  if (c.halo) return p == BF16 && conv_halo_ok(a, c.th, c.tw, c.bn);
   if (conv_tile_direct(c)) return p == BF16 && conv_dma_ok(a);
   if (a.split > 1) return false;  // only the LDS-DMA kernels split K
   return a.Cin % c.vec == 0 && a.Kp % CONV_KPAD == 0 && a.Cout % 8 == 0;
@@ -336,18 +340,20 @@ bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
 // Largest useful tile: prefer tiles that keep >= 2 workgroups per CU busy,
 // then the least padding waste, then the larger tile (more reuse per byte).
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus) {
+  int fam = -1;
+  for (int t = 0; t < conv_num_tiles(p); ++t)
+    if (conv_tile_ok(p, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(p, t)));
   int best = -1;
   double best_score = -1;
   for (int t = 0; t < conv_num_tiles(p); ++t) {
-    if (!conv_tile_ok(p, t, a)) continue;
+    if (!conv_tile_ok(p, t, a) || conv_tile_family(conv_tile(p, t)) != fam) continue;
     const ConvTile& c = conv_tile(p, t);
     const double tm = (a.M + c.bm - 1) / c.bm, tn = (a.Cout + c.bn - 1) / c.bn;
     const double wgs = tm * tn * a.Z;
     const double useful = (double)a.M * a.Cout / (tm * c.bm * tn * c.bn);
     const double fill = wgs >= 2.0 * num_cus ? 1.0 : wgs / (2.0 * num_cus);
     const double reuse = (double)c.bm * c.bn / (c.bm + c.bn) / 64.0;  // 1.0 for 128x128
-    const double score = useful * (0.35 + 0.65 * fill) * (0.6 + 0.4 * reuse) *
-                         (c.vec == 8 || p == F32 ? 1.0 : 0.9) * (conv_tile_direct(c) ? 1.5 : 1.0);
+    const double score = useful * (0.35 + 0.65 * fill) * (0.6 + 0.4 * reuse) * (c.vec == 8 || p == F32 ? 1.0 : 0.9);
     if (score > best_score) { best_score = score; best = t; }
   }
   return best;
@@ -363,6 +369,11 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
 }
 
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
+  if (p == BF16 && conv_tile(p, tile).halo) {
+    const ConvTile& c = conv_tile(p, tile);
+    launch_conv_halo(a, c.th, c.tw, c.bn, s);
+    return;
+  }
   if (p == BF16 && conv_tile_direct(conv_tile(p, tile))) {
     const ConvTile& c = conv_tile(p, tile);
     launch_conv_dma(a, c.bm, c.bn, c.waves, c.wgm, c.dma, s);

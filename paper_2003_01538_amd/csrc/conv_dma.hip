@@ -31,6 +31,8 @@
 #include "common.hpp"
 #include "device.hpp"
 
+#include <algorithm>
+
 namespace fs {
 
 namespace {
@@ -66,13 +68,15 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   }
 }
 
-// MFMAs of one 64-wide K-tile for a wave's TM x TN sub-tile (FM x FN blocks of
-// 32x32).  32x32x16 operands: lane l supplies row (l & 31), k-group (l >> 5)
-// of 8; the weights are the A operand, so block (i, j) accumulates D[n][m].
+// MFMAs of one 64-wide K-tile for a wave's FM x FN blocks of 32x32.
+// ra[i] / rb[j]: the LDS row this lane supplies for A block i / B block j.
+// 32x32x16 operands: lane l supplies row (l & 31) of its block, k-group
+// (l >> 5) of 8; the weights are the A operand, so block (i, j) accumulates
+// D[n][m].
 template <int FM, int FN>
-__device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int row_a, int row_b, int lane,
-                                          floatx16 (&acc)[FM][FN]) {
-  const int fr = lane & 31, fq = lane >> 5;
+__device__ __forceinline__ void mma_ktile_rows(const char* As, const char* Bs, const int (&ra)[FM],
+                                               const int (&rb)[FN], int lane, floatx16 (&acc)[FM][FN]) {
+  const int fq = lane >> 5;
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh) {  // two halves of the 64-wide K-tile
     bf16x8 af[2][FM], bfr[2][FN];
@@ -80,15 +84,9 @@ __device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int ro
     for (int ks = 0; ks < 2; ++ks) {
       const int c = (kh * 2 + ks) * 2 + fq;  // logical 16-byte chunk
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int r = row_a + i * 32 + fr;
-        af[ks][i] = *reinterpret_cast<const bf16x8*>(As + r * ROW + ((c ^ swz(r)) << 4));
-      }
+      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8*>(As + ra[i] * ROW + ((c ^ swz(ra[i])) << 4));
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int r = row_b + j * 32 + fr;
-        bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + r * ROW + ((c ^ swz(r)) << 4));
-      }
+      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + rb[j] * ROW + ((c ^ swz(rb[j])) << 4));
     }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
@@ -100,6 +98,19 @@ __device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int ro
   }
 }
 
+// The same for a wave sub-tile of consecutive rows row_a.., row_b...
+template <int FM, int FN>
+__device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int row_a, int row_b, int lane,
+                                          floatx16 (&acc)[FM][FN]) {
+  const int fr = lane & 31;
+  int ra[FM], rb[FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) ra[i] = row_a + i * 32 + fr;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) rb[j] = row_b + j * 32 + fr;
+  mma_ktile_rows<FM, FN>(As, Bs, ra, rb, lane, acc);
+}
+
 // Epilogue straight from the accumulators.  The MFMA computes D[n][m]
 // (weights as the A operand), so lane l holds pixel m = l & 31 and channels
 // 8g + 4q + r (q = l >> 5, r < 4) of each 32x32 block.  One permlane32 swap
@@ -107,16 +118,17 @@ __device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int ro
 // lanes 0-31 channels 8g.., lanes 32-63 channels 8(g+1).., for g = 0, 2.
 // Bias, residual, ReLU, bf16 rounding and a 16-byte store follow; with a K
 // split the raw fp32 sums go to the partial buffer instead.
+// mg[i]: the output row m (pixel) this lane holds in block i, or -1.
 template <int FM, int FN>
-__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)[FM][FN], int mrow, int ncol,
-                                              int z, int sp, int lane) {
-  const int fr = lane & 31, fq = lane >> 5;
+__device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&acc)[FM][FN], const int (&mg)[FM],
+                                                int ncol, int z, int sp, int lane) {
+  const int fq = lane >> 5;
   const float* __restrict__ bias = a.bias + z * a.b_mstride;
   const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
   uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
-    const int m = mrow + i * 32 + fr;
+    const int m = mg[i];
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
 #pragma unroll
@@ -130,7 +142,7 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)
           v[4 + r] = __uint_as_float(sw[1]);  // channels 8(gp+q) + 4 + r
         }
         const int n = ncol + j * 32 + 8 * (gp + fq);
-        if (m >= a.M || n >= a.Cout) continue;
+        if (m < 0 || m >= a.M || n >= a.Cout) continue;
         if (a.split > 1) {  // raw partial sums; the reduce kernel finishes
           float4* pp = reinterpret_cast<float4*>(a.partial + (((int64_t)sp * a.Z + z) * a.M + m) * a.Cout + n);
           pp[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -155,6 +167,15 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)
       }
     }
   }
+}
+
+template <int FM, int FN>
+__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)[FM][FN], int mrow, int ncol,
+                                              int z, int sp, int lane) {
+  int mg[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) mg[i] = mrow + i * 32 + (lane & 31);
+  conv_epilogue_m<FM, FN>(a, acc, mg, ncol, z, sp, lane);
 }
 
 // Tile of workgroup `bid` among tiles * Z * split, XCD-contiguous.
@@ -286,6 +307,387 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   conv_epilogue<FM, FN>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane);
 }
 
+// Direct 3x3 / stride 1 / pad 1 convolution with the input halo staged
+// once per 64-channel chunk.  The implicit GEMM above fetches every input
+// pixel once per filter tap (9 times for a 3x3 filter); here a workgroup
+// loads the (TH+2) x (W+2) patch of one 64-channel chunk into LDS once and
+// all 9 taps read their shifted A operands from it, while the weights of the
+// workgroup's BN output channels stay resident in LDS for its whole life.
+// The kernel is persistent: one workgroup per CU, each owning one (model,
+// N-tile) group and a contiguous range of its spatial tiles (TH output rows
+// x the full output width of one image); steps (tile, chunk) run through a
+// double-buffered patch, the next step's patch in flight while this one's
+// MFMAs run.  Each wave owns FM blocks of 32 pixels x all BN channels.  The
+// bias is loaded once; a tile's residual is loaded when its last step
+// starts, so neither waits at the epilogue.  Per output, the sum runs over
+// chunks, then taps, then the 64 channels in the same MFMA order as the
+// implicit GEMM; with one chunk (Cin = 64) the order, and so every bit, is
+// that of the implicit GEMM.
+template <int TH, int TW, int BN, int FM, int WBYTES>
+__global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvArgs a) {
+  constexpr int P = TH * TW, MB = P / 32, NW = MB / FM, FN = BN / 32;
+  constexpr int PW = TW + 2, NP = (TH + 2) * PW;  // patch width and pixels
+  constexpr int NPB = (NP + 7) / 8;               // 8-pixel load blocks
+  constexpr int PATCH = NPB * 8 * ROW;
+  constexpr int NIT = (NPB + NW - 1) / NW;        // patch load instructions per wave
+  static_assert(P % 32 == 0 && MB % FM == 0 && BN % 32 == 0, "tile");
+  __shared__ __attribute__((aligned(1024))) char smem[WBYTES + 2 * PATCH];
+  char* const wsm = smem;
+  char* const psm = smem + WBYTES;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane >> 3, fr = lane & 31, fq = lane >> 5;
+  const int CH = a.Cin / BK, nkt = a.Kp / BK;
+
+  // ---- this workgroup's group (model z, N-tile) and range of spatial tiles
+  const int tiles_h = (a.Ho + TH - 1) / TH, T = a.B * tiles_h;
+  const int NT = a.Cout / BN, G = a.Z * NT;
+  const int nwg = gridDim.x, base = nwg / G, rem = nwg % G, big = rem * (base + 1);
+  const int bx = blockIdx.x;
+  const int g = bx < big ? bx / (base + 1) : rem + (bx - big) / base;
+  const int gi = bx < big ? bx % (base + 1) : (bx - big) % base;
+  const int gsize = base + (g < rem ? 1 : 0);
+  const int z = g / NT, n0 = (g - z * NT) * BN;
+  const int t_begin = (int)((int64_t)gi * T / gsize), t_end = (int)((int64_t)(gi + 1) * T / gsize);
+  if (t_begin >= t_end) return;  // uniform over the workgroup
+
+  const __amdgpu_buffer_rsrc_t rx = rsrc(reinterpret_cast<const uint16_t*>(a.x) + z * a.x_mstride,
+                                         (uint32_t)((int64_t)a.B * a.H * a.W * a.Cin * 2));
+  const __amdgpu_buffer_rsrc_t rw = rsrc(reinterpret_cast<const uint16_t*>(a.w) + z * a.w_mstride,
+                                         (uint32_t)((int64_t)a.Cout * a.Kp * 2));
+
+  // ---- resident weights: LDS row kt * BN + n holds w[n0 + n][kt*64 .. +64]
+  {
+    const int nblk = nkt * BN / 8;
+    for (int blk = wave; blk < nblk; blk += NW) {
+      const int r = blk * 8 + lr;
+      const int kt = r / BN, n = r - kt * BN;
+      const int lc = (lane & 7) ^ swz(r);  // this lane fills physical chunk lane & 7
+      const uint32_t off = (uint32_t)((((int64_t)(n0 + n) * a.Kp) + kt * BK + lc * 8) * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void*)(wsm + blk * 1024), 16, off, 0, 0, 0);
+    }
+  }
+
+  // ---- patch loads: pixel q of the patch is input (oy0 - 1 + q / PW, q % PW - 1)
+  int q_dy[NIT], q_ix[NIT], q_lc[NIT];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int blk = it * NW + wave;
+    const int q = blk * 8 + lr;
+    q_lc[it] = (lane & 7) ^ swz(q);
+    if (blk < NPB && q < NP) {
+      const int pr = q / PW;
+      q_dy[it] = pr - 1;
+      q_ix[it] = q - pr * PW - 1;
+    } else {
+      q_dy[it] = -(1 << 28);  // never inside the image
+      q_ix[it] = 0;
+    }
+  }
+  auto issue_patch = [&](int t, int cc, int buf) {
+    const int img = t / tiles_h, oy0 = (t - img * tiles_h) * TH;
+    char* pb = psm + buf * PATCH;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int blk = it * NW + wave;
+      if (blk < NPB) {
+        const int iy = oy0 + q_dy[it], ix = q_ix[it];
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        const uint32_t off =
+            ok ? (uint32_t)(((((int64_t)img * a.H + iy) * a.W + ix) * a.Cin + cc * BK + q_lc[it] * 8) * 2) : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + blk * 1024), 16, off, 0, 0, 0);
+      }
+    }
+  };
+
+  // ---- this lane's pixels (block i of the wave is tile block wave * FM + i)
+  // and, for the epilogue, its 8-channel groups: after the permlane32 swap a
+  // lane holds channels n0 + 32 j + 8 (gp + fq) .. +8 of its pixel, gp = 0, 2
+  int q0[FM], pr_[FM], pc_[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int pidx = (wave * FM + i) * 32 + fr;
+    pr_[i] = pidx / TW;
+    pc_[i] = pidx - pr_[i] * TW;
+    q0[i] = pr_[i] * PW + pc_[i];
+  }
+  float bias_v[FN][2][8];
+  {
+    const float* __restrict__ bias = a.bias + z * a.b_mstride;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int n = n0 + j * 32 + 8 * (2 * h + fq);
+        const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+        const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+        bias_v[j][h][0] = b0.x; bias_v[j][h][1] = b0.y; bias_v[j][h][2] = b0.z; bias_v[j][h][3] = b0.w;
+        bias_v[j][h][4] = b1.x; bias_v[j][h][5] = b1.y; bias_v[j][h][6] = b1.z; bias_v[j][h][7] = b1.w;
+      }
+  }
+  const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
+  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
+
+  floatx16 acc[FM][FN];
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  };
+  zero_acc();
+  uint4 res_v[FM][FN][2];
+  int mg[FM];
+
+  const int steps = (t_end - t_begin) * CH;
+  issue_patch(t_begin, 0, 0);
+  for (int st = 0; st < steps; ++st) {
+    const int tj = st / CH, cc = st - tj * CH;
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (st + 1 < steps) {
+      const int tn = (st + 1) / CH;
+      issue_patch(t_begin + tn, st + 1 - tn * CH, (st + 1) & 1);
+    }
+    if (cc == CH - 1) {  // the tile's output rows and residual, ahead of the epilogue
+      const int t = t_begin + tj;
+      const int img = t / tiles_h, oy0 = (t - img * tiles_h) * TH;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int oy = oy0 + pr_[i];
+        mg[i] = oy < a.Ho ? (img * a.Ho + oy) * a.Wo + pc_[i] : -1;
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int n = n0 + j * 32 + 8 * (2 * h + fq);
+            res_v[i][j][h] = (res && mg[i] >= 0) ? *reinterpret_cast<const uint4*>(res + (int64_t)mg[i] * a.Cout + n)
+                                                  : uint4{0, 0, 0, 0};
+          }
+      }
+    }
+    const char* Pb = psm + (st & 1) * PATCH;
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) {
+      const int ky = tap / 3, kx = tap - ky * 3;
+      const int kt = tap * CH + cc;
+      int ra[FM], rb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) ra[i] = q0[i] + ky * PW + kx;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) rb[j] = kt * BN + j * 32 + fr;
+      mma_ktile_rows<FM, FN>(Pb, wsm, ra, rb, lane, acc);
+    }
+    if (cc == CH - 1) {  // epilogue: bias, residual, ReLU, bf16, 16-byte stores
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int gp = 2 * h;
+            float v[8], rr[8];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
+                                                               __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
+              v[r] = __uint_as_float(sw[0]);
+              v[4 + r] = __uint_as_float(sw[1]);
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += bias_v[j][h][e];
+            if (res) {
+              bf8_to_f8(res_v[i][j][h], rr);
+#pragma unroll
+              for (int e = 0; e < 8; ++e) v[e] += rr[e];
+            }
+            if (a.relu)
+#pragma unroll
+              for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+            const int n = n0 + j * 32 + 8 * (gp + fq);
+            if (mg[i] >= 0) *reinterpret_cast<uint4*>(y + (int64_t)mg[i] * a.Cout + n) = f8_to_bf8(v);
+          }
+      zero_acc();
+    }
+  }
+}
+
+// The ResNet stem fused: 7x7/2 conv in its space-to-depth form (4x4/1,
+// pad 2, on the [B][Hs][Ws][16] tensor, K = 256), bias, ReLU, bf16 rounding,
+// then the 3x3/2 max pool (pad 1), writing only the pooled tensor.  Rounding
+// before the max is exact: max commutes with a monotone rounding, so the
+// result equals the two layers run separately.
+//
+// A workgroup owns one (model, image, range of pooled rows).  It walks its
+// conv rows two at a time (one pooled row's worth): the 5 input rows a tile
+// needs are staged in LDS as 32-byte pixels (the two 16-byte halves of pixel
+// x are swapped when bit 3 of x is set, so the 16 consecutive pixels an
+// operand read touches fall on distinct banks), the 64 x 256 weights stay
+// resident, every 16-wide K step is one (Ky, Kx) tap with the MFMA order of
+// the implicit GEMM, and the activated conv rows go to a ring of three LDS
+// row buffers (row r in buffer r % 3), from which the pooled row is taken.
+// A range that does not start at the top first computes the conv row just
+// above it.  7 waves: one 32-pixel block x 64 channels each (2 rows x 112).
+constexpr int STEM_WMAX = 112;                 // conv output width limit
+constexpr int STEM_PW = STEM_WMAX + 3;         // patch pixels per row
+constexpr int STEM_PATCH = ((5 * STEM_PW * 32 + 1023) / 1024) * 1024;
+constexpr int STEM_WAVES = (2 * STEM_WMAX + 31) / 32;
+constexpr int STEM_ROWS_PER_WG = 7;            // pooled rows per workgroup
+
+__global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
+  constexpr int WB = 4 * 64 * ROW;             // resident weights
+  constexpr int RB = STEM_WMAX * ROW;          // one activated conv row
+  __shared__ __attribute__((aligned(1024))) char smem[WB + 2 * STEM_PATCH + 3 * RB];
+  char* const wsm = smem;
+  char* const psm = smem + WB;
+  char* const rsm = psm + 2 * STEM_PATCH;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane >> 3, fr = lane & 31, fq = lane >> 5;
+  const int Wc = a.Wo, Hc = a.Ho;              // conv output
+  const int Hp = (Hc - 1) / 2 + 1, Wp = (Wc - 1) / 2 + 1;  // 3x3/2/p1 pool output
+  const int PWc = Wc + 3;
+  const int nranges = (Hp + STEM_ROWS_PER_WG - 1) / STEM_ROWS_PER_WG;
+  const int ri = blockIdx.x % nranges, zb = blockIdx.x / nranges;
+  const int b = zb % a.B, z = zb / a.B;
+  const int py0 = ri * STEM_ROWS_PER_WG, py1 = min(Hp, py0 + STEM_ROWS_PER_WG);
+  const int first = py0 > 0 ? -1 : 0;          // tile -1 computes conv rows 2*py0 - 2, 2*py0 - 1
+  const int ntiles = py1 - py0 - first;
+
+  const __amdgpu_buffer_rsrc_t rx = rsrc(reinterpret_cast<const uint16_t*>(a.x) + z * a.x_mstride,
+                                         (uint32_t)((int64_t)a.B * a.H * a.W * 16 * 2));
+  const __amdgpu_buffer_rsrc_t rw = rsrc(reinterpret_cast<const uint16_t*>(a.w) + z * a.w_mstride,
+                                         (uint32_t)((int64_t)a.Cout * a.Kp * 2));
+  // resident weights: LDS row Ky * 64 + n holds w[n][Ky*64 .. +64]
+  for (int blk = wave; blk < 4 * 64 / 8; blk += STEM_WAVES) {
+    const int r = blk * 8 + lr;
+    const int ky = r >> 6, n = r & 63;
+    const int lc = (lane & 7) ^ swz(r);
+    const uint32_t off = (uint32_t)(((int64_t)n * a.Kp + ky * BK + lc * 8) * 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void*)(wsm + blk * 1024), 16, off, 0, 0, 0);
+  }
+  // patch of the tile with top conv row rho0: input rows rho0 - 2 .. rho0 + 2,
+  // columns -2 .. Wc; 16-byte slot s = 2 * (pr * PWc + pc) + stored half
+  const int nslot = 5 * PWc * 2;
+  auto issue_patch = [&](int rho0, int buf) {
+    char* pb = psm + buf * STEM_PATCH;
+    for (int blk = wave; blk * 64 < nslot; blk += STEM_WAVES) {
+      const int sl = blk * 64 + lane;
+      uint32_t off = OOB;
+      if (sl < nslot) {
+        const int pix = sl >> 1, pr = pix / PWc, pc = pix - pr * PWc;
+        const int h = (sl & 1) ^ ((pc >> 3) & 1);
+        const int iy = rho0 - 2 + pr, ix = pc - 2;
+        if ((unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W)
+          off = (uint32_t)(((((int64_t)b * a.H + iy) * a.W + ix) * 16 + h * 8) * 2);
+      }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + blk * 1024), 16, off, 0, 0, 0);
+    }
+  };
+
+  // this lane's pixel in the 2-row tile
+  const int pidx = wave * 32 + fr;
+  const bool pv = pidx < 2 * Wc;
+  const int pr0 = pv ? pidx / Wc : 0, pc0 = pv ? pidx - pr0 * Wc : 0;
+  float bias_v[2][2][8];
+  {
+    const float* __restrict__ bias = a.bias + z * a.b_mstride;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bias_v[j][h][e] = bias[j * 32 + 8 * (2 * h + fq) + e];
+  }
+  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
+
+  issue_patch(2 * (py0 + first), 0);
+  for (int st = 0; st < ntiles; ++st) {
+    const int py = py0 + first + st, rho0 = 2 * py;
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (st + 1 < ntiles) issue_patch(rho0 + 2, (st + 1) & 1);
+    const char* Pb = psm + (st & 1) * STEM_PATCH;
+    floatx16 acc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+#pragma unroll
+    for (int ky = 0; ky < 4; ++ky) {
+      bf16x8 af[4], bfr[4][2];
+#pragma unroll
+      for (int kx = 0; kx < 4; ++kx) {
+        const int pc = pc0 + kx;
+        const int slot = 2 * ((pr0 + ky) * PWc + pc) + (fq ^ ((pc >> 3) & 1));
+        af[kx] = *reinterpret_cast<const bf16x8*>(Pb + slot * 16);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int r = ky * 64 + j * 32 + fr;
+          bfr[kx][j] = *reinterpret_cast<const bf16x8*>(wsm + r * ROW + (((2 * kx + fq) ^ swz(r)) << 4));
+        }
+      }
+#pragma unroll
+      for (int kx = 0; kx < 4; ++kx)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kx][j], af[kx], acc[j], 0, 0, 0);
+    }
+    // activated bf16 conv rows into the LDS ring (row rho in buffer rho % 3)
+    const int rho = rho0 + pr0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int gp = 2 * h;
+        float v[8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[j][gp * 4 + r]),
+                                                           __float_as_uint(acc[j][(gp + 1) * 4 + r]), false, false);
+          v[r] = __uint_as_float(sw[0]);
+          v[4 + r] = __uint_as_float(sw[1]);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias_v[j][h][e], 0.f);
+        const int chunk = j * 4 + gp + fq;  // 8-channel group of the 64
+        if (pv && rho >= 0 && rho < Hc)
+          *reinterpret_cast<uint4*>(rsm + (rho % 3) * RB + pc0 * ROW + ((chunk ^ swz(pc0)) << 4)) = f8_to_bf8(v);
+      }
+    if (st == 0 && first < 0) continue;  // the row above the range only
+    __syncthreads();
+    // pooled row py: conv rows 2py-1 .. 2py+1, columns 2px-1 .. 2px+1
+    for (int item = tid; item < Wp * 8; item += 64 * STEM_WAVES) {
+      const int px = item >> 3, ch = item & 7;
+      float m[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
+      for (int dy = -1; dy <= 1; ++dy) {
+        const int cr = rho0 + dy;
+        if (cr < 0 || cr >= Hc) continue;
+        for (int dx = -1; dx <= 1; ++dx) {
+          const int cc = 2 * px + dx;
+          if (cc < 0 || cc >= Wc) continue;
+          float q[8];
+          bf8_to_f8(*reinterpret_cast<const uint4*>(rsm + (cr % 3) * RB + cc * ROW + ((ch ^ swz(cc)) << 4)), q);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) m[e] = fmaxf(m[e], q[e]);
+        }
+      }
+      *reinterpret_cast<uint4*>(y + (((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) = f8_to_bf8(m);
+    }
+  }
+}
+
+bool stem_pool_ok_impl(const ConvArgs& a) {
+  return a.Cin == 16 && a.kh == 4 && a.kw == 4 && a.stride == 1 && a.pad == 2 && a.Cout == 64 && a.Kp == 256 &&
+         a.K == 256 && a.Wo <= STEM_WMAX && a.Wo >= 1 && a.Ho >= 1 && a.relu && !a.res && a.Wo == a.W &&
+         a.Ho == a.H;
+}
+
 // Split-K completion: partial sums added in split order, then bias,
 // residual, ReLU and the bf16 store, 8 channels per thread.
 __global__ void __launch_bounds__(256) k_conv_splitk_reduce(ConvArgs a) {
@@ -349,6 +751,54 @@ int conv_split(Prec p, const ConvArgs& a, int num_cus) {
 bool conv_dma_ok(const ConvArgs& a) {
   const bool tiles_ok = a.Cin % BK == 0 || (a.Cin % 8 == 0 && BK % a.Cin == 0 && (a.kw * a.Cin) % BK == 0);
   return tiles_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0;
+}
+
+// Halo kernel shapes: TH output rows x TW (= the output width) pixels, BN
+// output channels, FM M-blocks per wave, resident weights <= 72 KB.
+constexpr int HALO_WBYTES = 72 * 1024;
+
+bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn) {
+  return a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin % BK == 0 && a.K == a.Kp &&
+         a.Wo == tw && a.Ho == a.H && a.Wo == a.W && a.Cout % bn == 0 && a.split == 1 &&
+         (int64_t)a.Kp * bn * 2 <= HALO_WBYTES && a.Z * (a.Cout / bn) <= 4096;
+}
+
+static int cus_of_current_device() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cache[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+void launch_conv_halo(const ConvArgs& a_in, int th, int tw, int bn, hipStream_t s) {
+  ConvArgs a = a_in;  // the halo kernel never splits K: it always writes finished outputs
+  a.split = 1;
+  a.partial = nullptr;
+  const int groups = a.Z * (a.Cout / bn);
+  const int tiles = a.B * ((a.Ho + th - 1) / th) * groups;
+  const int nwg = std::max(groups, std::min(tiles, cus_of_current_device()));
+#define FS_HALO(THv, TWv, BNv, FMv)                                                                            \
+  if (th == THv && tw == TWv && bn == BNv) {                                                                   \
+    hipLaunchKernelGGL((k_conv_halo<THv, TWv, BNv, FMv, HALO_WBYTES>), dim3(nwg), dim3(64 * (THv * TWv / 32) / FMv), \
+                       0, s, a);                                                                               \
+    return;                                                                                                    \
+  }
+  FS_HALO(4, 56, 64, 1)
+#undef FS_HALO
+}
+
+bool conv_stem_pool_ok(const ConvArgs& a) { return stem_pool_ok_impl(a); }
+
+// y: the pooled [B][Hp][Wp][64] tensor; a.Ho x a.Wo is the conv output size.
+void launch_conv_stem_pool(const ConvArgs& a, hipStream_t s) {
+  const int Hp = (a.Ho - 1) / 2 + 1;
+  const int nranges = (Hp + STEM_ROWS_PER_WG - 1) / STEM_ROWS_PER_WG;
+  hipLaunchKernelGGL(k_stem_pool, dim3(a.Z * a.B * nranges), dim3(64 * STEM_WAVES), 0, s, a);
 }
 
 void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s) {

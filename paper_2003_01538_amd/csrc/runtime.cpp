@@ -117,6 +117,8 @@ struct LayerPlan {
   int in_slot = SLOT_INPUT, res_slot = -1, out_slot = -1;
   bool last = false;
   bool s2d = false;       // first conv rewritten on the space-to-depth input
+  bool pool_fused = false;  // conv: also applies the next layer's 3x3/2 max pool, writes the pooled tensor
+  bool fused_away = false;  // max pool: done by the conv before it (no launch, shares its slot)
   int kreal = 0;          // kh * kw * cin of the layer as specified (FLOP count)
   int in_c_real = 0;      // input channels as specified (byte count)
 };
@@ -418,6 +420,12 @@ void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
         } else if (L.src < 0) {
           e->need_plain = true;
         }
+        if (P.s2d && L.relu && L.residual_src < 0 && L.cout == 64 && P.kh == 4 && P.pad == 2 && P.Kp == 256 &&
+            P.out.W <= 112 && P.out.H == P.in.H && P.out.W == P.in.W && i + 1 < n - 1) {
+          const fs_layer& Nx = s.layers[i + 1];  // a max pool that is the conv's only reader
+          P.pool_fused = Nx.op == FS_OP_MAXPOOL && Nx.src == i && Nx.kh == 3 && Nx.kw == 3 && Nx.stride == 2 &&
+                         Nx.pad == 1 && last_use[i] == i + 1;
+        }
         break;
       case FS_OP_MAXPOOL:
         P.out = Shape{(P.in.H + 2 * L.pad - L.kh) / L.stride + 1, (P.in.W + 2 * L.pad - L.kw) / L.stride + 1, P.in.C};
@@ -436,10 +444,19 @@ void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
     P.res_slot = P.res >= 0 ? layer_slot[P.res] : -1;
     // free slots whose readers are all at or before this layer... but not
     // before this layer has read them: release after assigning the output.
-    if (P.last) {
+    if (P.op == FS_OP_MAXPOOL && L.src == i - 1 && i > 0 && g.layers[i - 1].pool_fused) {
+      // computed by the conv before it, straight into that conv's slot
+      P.fused_away = true;
+      const int slot = g.layers[i - 1].out_slot;
+      P.out_slot = slot;
+      layer_slot[i] = slot;
+      slot_elems[slot] = std::max(slot_elems[slot], P.out.elems());
+      slot_busy_until[slot] = std::max(slot_busy_until[slot], std::max(last_use[i], i));
+    } else if (P.last) {
       P.out_slot = SLOT_LOGITS;
     } else {
-      const int64_t need = P.out.elems();
+      const int64_t need = P.pool_fused ? (int64_t)((P.out.H - 1) / 2 + 1) * ((P.out.W - 1) / 2 + 1) * P.out.C
+                                        : P.out.elems();
       int pick = -1;
       for (size_t sidx = 0; sidx < slot_busy_until.size(); ++sidx) {
         if (slot_busy_until[sidx] < i) {  // free: its last reader ran before layer i
@@ -652,7 +669,7 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
     choice[gi].assign(g.layers.size(), -1);
     for (size_t li = 0; li < g.layers.size(); ++li) {
       LayerPlan& P = g.layers[li];
-      if (P.op != FS_OP_CONV) continue;
+      if (P.op != FS_OP_CONV || P.pool_fused) continue;
       ConvArgs a = conv_args(e, g, P, bucket, slot_ptr(g, P.out_slot), (int64_t)g.slot_elems[P.out_slot] * e->max_batch);
       const size_t need = conv_partial_floats(a) * 4;
       if (need > e->conv_partial.bytes) {  // split-K scratch for this bucket
@@ -661,14 +678,14 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
         e->workspace_bytes += (int64_t)e->conv_partial.bytes;
         a.partial = static_cast<float*>(e->conv_partial.p);
       }
-      bool any_dma = false;
+      int fam = -1;  // the layer runs in the highest kernel family that fits it
       for (int t = 0; t < conv_num_tiles(e->prec); ++t)
-        if (conv_tile_ok(e->prec, t, a) && conv_tile_direct(conv_tile(e->prec, t))) any_dma = true;
+        if (conv_tile_ok(e->prec, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(e->prec, t)));
       int best = conv_pick_tile(e->prec, a, e->num_cus);
       if (e->tune) {
         float best_ms = 1e30f;
         for (int t = 0; t < conv_num_tiles(e->prec); ++t) {
-          if (!conv_tile_ok(e->prec, t, a) || conv_tile_direct(conv_tile(e->prec, t)) != any_dma) continue;
+          if (!conv_tile_ok(e->prec, t, a) || conv_tile_family(conv_tile(e->prec, t)) != fam) continue;
           launch_conv(a, e->prec, t, s);
           HIPCHK(hipEventRecord(e0, s));
           launch_conv(a, e->prec, t, s);
@@ -742,17 +759,22 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           const ConvArgs a = conv_args(e, g, P, B, y, y_ms);
           const int tile = tiles[gi][li];
           launch.M = a.M; launch.N = a.Cout; launch.K = P.kreal;
-          launch.kernel = conv_tile(p, tile).name;
+          launch.kernel = P.pool_fused ? "stem_s2d_conv_maxpool" : conv_tile(p, tile).name;
           const double kreal = (double)P.kreal;
           const double flops = 2.0 * a.M * a.Cout * kreal * g.Z;
           const double in_b = (double)B * P.in.H * P.in.W * P.in_c_real * (P.s2d ? 4 : 1) * esz *
                               (P.in_slot == SLOT_INPUT ? 1 : g.Z);
-          const double bytes = in_b + ((double)a.Cout * kreal * esz + (double)a.M * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
-          launch(K_CONV, flops, bytes, a.split > 1 ? 2 : 1, [&] { launch_conv(a, p, tile, s); });
+          const double out_px = P.pool_fused ? (double)B * ((P.out.H - 1) / 2 + 1) * ((P.out.W - 1) / 2 + 1) : a.M;
+          const double bytes = in_b + ((double)a.Cout * kreal * esz + out_px * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
+          if (P.pool_fused)
+            launch(K_CONV, flops, bytes, 1, [&] { launch_conv_stem_pool(a, s); });
+          else
+            launch(K_CONV, flops, bytes, a.split > 1 ? 2 : 1, [&] { launch_conv(a, p, tile, s); });
           break;
         }
         case FS_OP_MAXPOOL:
         case FS_OP_GAP: {
+          if (P.fused_away) break;
           PoolArgs a{};
           a.x = x; a.x_mstride = x_ms; a.y = y; a.y_mstride = y_ms;
           a.B = B; a.H = P.in.H; a.W = P.in.W; a.C = P.in.C;
@@ -809,8 +831,8 @@ int launches_per_pass(fs_ensemble* e) {
       if (P.op == FS_OP_FC)
         n += fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus));
       else if (P.op == FS_OP_CONV)
-        n += conv_args(e, g, P, e->max_batch, nullptr, 0).split > 1 ? 2 : 1;
-      else
+        n += (!P.pool_fused && conv_args(e, g, P, e->max_batch, nullptr, 0).split > 1) ? 2 : 1;
+      else if (!P.fused_away)
         n += 1;
     }
   return n;
@@ -1153,10 +1175,14 @@ fs_status fs_test_preprocess(const fs_image* imgs, int32_t B, int32_t out_h, int
   });
 }
 
-fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t Cin, const float* w,
-                       const float* bias, const float* res, int32_t Cout, int32_t kh, int32_t kw, int32_t stride,
-                       int32_t pad, int32_t relu, int32_t precision, int32_t tile, float* out, int32_t device) {
-  return guarded(nullptr, [&] {
+// One conv on host tensors; with stem_pool the space-to-depth stem kernel
+// that also applies the 3x3/2/p1 max pool runs instead, and out receives
+// the pooled tensor.
+static void run_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t Cin, const float* w,
+                          const float* bias, const float* res, int32_t Cout, int32_t kh, int32_t kw, int32_t stride,
+                          int32_t pad, int32_t relu, int32_t precision, int32_t tile, float* out, int32_t device,
+                          bool stem_pool) {
+  {
     Prec p = prec_of(precision);
     if (!in || !w || !out || B < 1 || H < 1 || W < 1 || Cin < 1 || Cout < 1 || kh < 1 || kw < 1 || stride < 1 ||
         pad < 0)
@@ -1218,6 +1244,15 @@ fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t
     a.B = B; a.H = gH; a.W = gW; a.Cin = gC; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
     a.kh = gk; a.kw = gk; a.stride = gs; a.pad = gp; a.relu = relu ? 1 : 0;
     a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = 1;
+    if (stem_pool) {
+      if (!use_s2d || !conv_stem_pool_ok(a)) fail(FS_ERR_UNSUPPORTED, "not a space-to-depth stem the fused kernel takes");
+      const int64_t npool = (int64_t)B * ((Ho - 1) / 2 + 1) * ((Wo - 1) / 2 + 1) * Cout;
+      launch_conv_stem_pool(a, nullptr);
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipDeviceSynchronize());
+      download_as(out, dy, npool, p);
+      return;
+    }
     int tl = tile;
     if (tl < 0) tl = conv_pick_tile(p, a, num_cus_of(device));
     if (!conv_tile_ok(p, tl, a)) fail(FS_ERR_UNSUPPORTED, "tile " + std::to_string(tile) + " does not fit this conv");
@@ -1229,6 +1264,23 @@ fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t
     HIPCHK(hipGetLastError());
     HIPCHK(hipDeviceSynchronize());
     download_as(out, dy, no, p);
+  }
+}
+
+fs_status fs_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int32_t Cin, const float* w,
+                       const float* bias, const float* res, int32_t Cout, int32_t kh, int32_t kw, int32_t stride,
+                       int32_t pad, int32_t relu, int32_t precision, int32_t tile, float* out, int32_t device) {
+  return guarded(nullptr, [&] {
+    run_test_conv(in, B, H, W, Cin, w, bias, res, Cout, kh, kw, stride, pad, relu, precision, tile, out, device,
+                  false);
+  });
+}
+
+fs_status fs_test_stem_pool(const float* in, int32_t B, int32_t H, int32_t W, const float* w, const float* bias,
+                            float* out, int32_t device) {
+  return guarded(nullptr, [&] {
+    if (H % 2 || W % 2) fail(FS_ERR_UNSUPPORTED, "the space-to-depth stem needs even H and W");
+    run_test_conv(in, B, H, W, 3, w, bias, nullptr, 64, 7, 7, 2, 3, 1, FS_BF16, -1, out, device, true);
   });
 }
 

@@ -106,6 +106,8 @@ SIGNATURES = [
                                     _fp, _fp, _fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, _fp, ctypes.c_int32]),
+    ("fs_test_stem_pool", ctypes.c_int, [_fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _fp, _fp, _fp,
+                                         ctypes.c_int32]),
     ("fs_test_maxpool", ctypes.c_int, [_fp] + [ctypes.c_int32] * 8 + [_fp, ctypes.c_int32]),
     ("fs_test_gap", ctypes.c_int, [_fp] + [ctypes.c_int32] * 5 + [_fp, ctypes.c_int32]),
     ("fs_test_fc", ctypes.c_int, [_fp, ctypes.c_int32, ctypes.c_int32, _fp, _fp, ctypes.c_int32,
@@ -315,6 +317,17 @@ def fs_test_conv(x, w, bias, res, stride, pad, relu, precision, tile=-1, device=
     r = None if res is None else np.ascontiguousarray(res, np.float32)
     _check(load().fs_test_conv(_f(x), B, H, W, Cin, _f(w), _f(b), _f(r), Cout, kh, kw, stride, pad,
                                int(relu), precision, tile, _f(out), device))
+    return out
+
+
+def fs_test_stem_pool(x, w, bias, device=0):
+    x = np.ascontiguousarray(x, np.float32)
+    w = np.ascontiguousarray(w, np.float32)
+    B, H, W, _ = x.shape
+    Ho, Wo = H // 2, W // 2
+    out = np.zeros((B, (Ho - 1) // 2 + 1, (Wo - 1) // 2 + 1, 64), np.float32)
+    b = None if bias is None else np.ascontiguousarray(bias, np.float32)
+    _check(load().fs_test_stem_pool(_f(x), B, H, W, _f(w), _f(b), _f(out), device))
     return out
 
 

@@ -92,6 +92,8 @@ CONV_CASES = [
     (1, 7, 7, 256, 512, 3, 1, 1, 0, 1),    # deep layer, residual, no ReLU
     (2, 9, 9, 128, 256, 1, 1, 0, 1, 1),    # bottleneck expand + residual
     (1, 5, 6, 16, 32, 3, 1, 1, 1, 0),      # tiny-net second conv
+    (2, 12, 56, 64, 64, 3, 1, 1, 1, 1),    # halo kernel, 4-row tiles of width 56
+    (3, 10, 56, 64, 64, 3, 1, 1, 0, 0),    # halo kernel, partial last row tile, no residual / ReLU
 ]
 
 
@@ -129,7 +131,7 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
     o, ab = oracle.conv2d(x, w, b, s, p, relu, r, PREC[prec], want_abs=True)
     tiles = _tiles_for(prec, Cin)
     assert tiles
-    ran = 0
+    ran, ran_names = 0, []
     for t in tiles + [-1]:
         try:
             g = fsb.fs_test_conv(x, w, b, r, s, p, relu, prec, tile=t)
@@ -137,6 +139,7 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
             assert e.status == fsb.FS_ERR_UNSUPPORTED and t >= 0
             continue
         ran += 1
+        ran_names.append(fsb.fs_conv_tile_name(prec, t) if t >= 0 else "auto")
         if prec == BF16:
             assert_bf16_close(g, o, ab, what=f"case {ci} tile {t}")
         else:
@@ -144,6 +147,21 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
     assert ran >= 2
     if prec == BF16 and Cin % 64 == 0:  # the LDS-DMA kernels ran on this shape
         assert ran >= 2 + sum(1 for t in tiles if "dma" in fsb.fs_conv_tile_name(prec, t))
+    if prec == BF16 and k == 3 and s == 1 and Cin == 64 and Cout % 64 == 0 and W == 56:  # and the halo kernel
+        assert any("halo" in n for n in ran_names), ran_names
+
+
+def _tile_index(name_part):
+    return next(t for t in range(fsb.fs_conv_num_tiles(BF16)) if name_part in fsb.fs_conv_tile_name(BF16, t))
+
+
+def test_halo_kernel_bits_equal_implicit_gemm_for_one_chunk(gpu_lib):
+    # With Cin = 64 the halo kernel sums each output over the taps in the
+    # implicit GEMM's K order with the same MFMA sequence: identical bits.
+    x, w, b, r = _conv_inputs(CONV_CASES[-2], BF16, 17)  # 12 x 56, Cin 64, residual
+    g_halo = fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16, tile=_tile_index("halo_4x56"))
+    g_dma = fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16, tile=_tile_index("dma2_128x64"))
+    assert np.array_equal(g_halo.view(np.uint32), g_dma.view(np.uint32))
 
 
 def test_conv_repeat_is_bit_identical(gpu_lib):
@@ -151,6 +169,24 @@ def test_conv_repeat_is_bit_identical(gpu_lib):
     g0 = fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16)
     for _ in range(5):
         assert np.array_equal(fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16), g0)
+
+
+@pytest.mark.parametrize("B,H,W", [(2, 32, 32), (1, 224, 224), (3, 30, 20), (1, 2, 6)])
+def test_stem_conv_maxpool_fused(gpu_lib, B, H, W):
+    # the fused stem equals the conv and the max pool run separately, bit for
+    # bit (same sums, and max commutes with the bf16 rounding), and the oracle
+    rng = np.random.default_rng(H * 1000 + W)
+    x = oracle.round_bf16(rng.standard_normal((B, H, W, 3)).astype(np.float32))
+    w = oracle.round_bf16((rng.standard_normal((64, 7, 7, 3)) * np.sqrt(2.0 / 147)).astype(np.float32))
+    b = (rng.standard_normal(64) * 0.1).astype(np.float32)
+    g = fsb.fs_test_stem_pool(x, w, b)
+    sep = fsb.fs_test_maxpool(fsb.fs_test_conv(x, w, b, None, 2, 3, 1, BF16), 3, 2, 1, BF16)
+    assert g.shape == sep.shape
+    assert np.array_equal(g.view(np.uint32), sep.view(np.uint32))
+    c, ab = oracle.conv2d(x, w, b, 2, 3, 1, None, "bf16", want_abs=True)
+    o = oracle.maxpool(c, 3, 2, 1)
+    abp = oracle.maxpool(ab, 3, 2, 1)  # a bound for whichever window element won
+    assert_bf16_close(g, o, abp, frac_exact=0.99, what=f"stem {B}x{H}x{W}")
 
 
 # -------------------------------------------------------------------- pooling
