@@ -38,6 +38,7 @@ namespace fs {
 namespace {
 
 typedef __attribute__((address_space(3))) void lds_void;
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 64;          // bf16 elements per K-tile row (128 bytes)
 constexpr int ROW = 128;        // LDS bytes per tile row
@@ -54,6 +55,17 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// s_waitcnt lgkmcnt(0), leaving vmcnt and expcnt alone
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4)); }
+
+// Workgroup barrier without a memory fence (so it does not wait for vector
+// memory operations); the compiler may not move memory accesses across it.
+__device__ __forceinline__ void wg_barrier() {
+  __asm__ __volatile__("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  __asm__ __volatile__("" ::: "memory");
 }
 
 // Wait until at most `ahead` K-tiles (LPT load instructions each) of this
@@ -427,7 +439,6 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
       }
   }
   const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
-  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
 
   floatx16 acc[FM][FN];
   auto zero_acc = [&]() {
@@ -442,17 +453,23 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
   uint4 res_v[FM][FN][2];
   int mg[FM];
 
+  // outputs through a buffer resource: an epilogue issues exactly NSTORE
+  // stores per lane (out-of-range ones are dropped), so the next step waits
+  // for its patch without waiting for them
+  constexpr int NSTORE = FM * FN * 2;
+  const __amdgpu_buffer_rsrc_t ry = rsrc(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride,
+                                         (uint32_t)((int64_t)a.M * a.Cout * 2));
   const int steps = (t_end - t_begin) * CH;
   issue_patch(t_begin, 0, 0);
+  // every step ends with NSTORE stores (dropped ones where no tile ends), so
+  // every step starts with the same count of stores in flight behind its patch
+#pragma unroll
+  for (int u = 0; u < NSTORE; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
   for (int st = 0; st < steps; ++st) {
     const int tj = st / CH, cc = st - tj * CH;
-    wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    if (st + 1 < steps) {
-      const int tn = (st + 1) / CH;
-      issue_patch(t_begin + tn, st + 1 - tn * CH, (st + 1) & 1);
-    }
-    if (cc == CH - 1) {  // the tile's output rows and residual, ahead of the epilogue
+    wait_vmcnt<NSTORE>();  // the patch landed; the last step's stores may be in flight
+    wg_barrier();
+    if (cc == CH - 1) {  // the tile's output rows and residual, requested before the next patch
       const int t = t_begin + tj;
       const int img = t / tiles_h, oy0 = (t - img * tiles_h) * TH;
 #pragma unroll
@@ -469,6 +486,10 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
           }
       }
     }
+    if (st + 1 < steps) {
+      const int tn = (st + 1) / CH;
+      issue_patch(t_begin + tn, st + 1 - tn * CH, (st + 1) & 1);
+    }
     const char* Pb = psm + (st & 1) * PATCH;
 #pragma unroll
     for (int tap = 0; tap < 9; ++tap) {
@@ -481,7 +502,10 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
       for (int j = 0; j < FN; ++j) rb[j] = kt * BN + j * 32 + fr;
       mma_ktile_rows<FM, FN>(Pb, wsm, ra, rb, lane, acc);
     }
-    if (cc == CH - 1) {  // epilogue: bias, residual, ReLU, bf16, 16-byte stores
+    if (cc != CH - 1) {
+#pragma unroll
+      for (int u = 0; u < NSTORE; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
+    } else {  // epilogue: bias, residual, ReLU, bf16, 16-byte stores
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -508,7 +532,8 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
 #pragma unroll
               for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
             const int n = n0 + j * 32 + 8 * (gp + fq);
-            if (mg[i] >= 0) *reinterpret_cast<uint4*>(y + (int64_t)mg[i] * a.Cout + n) = f8_to_bf8(v);
+            const uint32_t off = mg[i] >= 0 ? (uint32_t)(((int64_t)mg[i] * a.Cout + n) * 2) : OOB;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry, off, 0, 0);
           }
       zero_acc();
     }
@@ -521,29 +546,39 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
 // before the max is exact: max commutes with a monotone rounding, so the
 // result equals the two layers run separately.
 //
-// A workgroup owns one (model, image, range of pooled rows).  It walks its
-// conv rows two at a time (one pooled row's worth): the 5 input rows a tile
-// needs are staged in LDS as 32-byte pixels (the two 16-byte halves of pixel
-// x are swapped when bit 3 of x is set, so the 16 consecutive pixels an
-// operand read touches fall on distinct banks), the 64 x 256 weights stay
-// resident, every 16-wide K step is one (Ky, Kx) tap with the MFMA order of
-// the implicit GEMM, and the activated conv rows go to a ring of three LDS
-// row buffers (row r in buffer r % 3), from which the pooled row is taken.
-// A range that does not start at the top first computes the conv row just
-// above it.  7 waves: one 32-pixel block x 64 channels each (2 rows x 112).
+// Persistent: the workgroups are split evenly over the models, and each
+// walks a contiguous run of (image, pooled-row pair) steps of its model with
+// that model's 64 x 256 weights resident in LDS.  A step computes 4 conv rows
+// (2 pooled rows' worth) from the 7 input rows it needs, staged in LDS as
+// 32-byte pixels (the two 16-byte halves of pixel x are swapped when bit 3
+// of x is set, so the 16 consecutive pixels an operand read touches fall on
+// distinct banks) and double-buffered: the next step's rows load while this
+// step's MFMAs run.  Every 16-wide K step is one (Ky, Kx) tap, in the MFMA
+// order of the implicit GEMM.  The activated rows go to a ring of five LDS
+// row buffers (conv row r in buffer r % 5), from which the two pooled rows
+// are taken; the last conv row stays for the next pair.  A run that starts
+// below the top of an image first computes the four conv rows above it.
+// 7 waves, each two 32-pixel blocks x 64 channels (4 rows x 112 = 14 blocks).
 constexpr int STEM_WMAX = 112;                 // conv output width limit
 constexpr int STEM_PW = STEM_WMAX + 3;         // patch pixels per row
-constexpr int STEM_PATCH = ((5 * STEM_PW * 32 + 1023) / 1024) * 1024;
-constexpr int STEM_WAVES = (2 * STEM_WMAX + 31) / 32;
-constexpr int STEM_ROWS_PER_WG = 7;            // pooled rows per workgroup
+constexpr int STEM_TR = 4;                     // conv rows per step
+constexpr int STEM_PR = STEM_TR + 3;           // input rows per step
+constexpr int STEM_RING = STEM_TR + 1;         // conv rows kept for pooling
+constexpr int STEM_PATCH = ((STEM_PR * STEM_PW * 32 + 1023) / 1024) * 1024;
+constexpr int STEM_FM = 2;                     // 32-pixel blocks per wave
+constexpr int STEM_WAVES = (STEM_TR * STEM_WMAX + 32 * STEM_FM - 1) / (32 * STEM_FM);
 
 __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
   constexpr int WB = 4 * 64 * ROW;             // resident weights
   constexpr int RB = STEM_WMAX * ROW;          // one activated conv row
-  __shared__ __attribute__((aligned(1024))) char smem[WB + 2 * STEM_PATCH + 3 * RB];
-  char* const wsm = smem;
-  char* const psm = smem + WB;
-  char* const rsm = psm + 2 * STEM_PATCH;
+  // separate arrays (and a step loop unrolled by two, so each step reads one
+  // patch buffer and fills the other by name): the compiler can then tell
+  // that the LDS reads and writes of a step do not touch the buffer the
+  // direct loads are filling, and does not wait for those loads
+  __shared__ __attribute__((aligned(1024))) char wsm[WB];
+  __shared__ __attribute__((aligned(1024))) char psm0[STEM_PATCH];
+  __shared__ __attribute__((aligned(1024))) char psm1[STEM_PATCH];
+  __shared__ __attribute__((aligned(1024))) char rsm[STEM_RING * RB];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -551,12 +586,25 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
   const int Wc = a.Wo, Hc = a.Ho;              // conv output
   const int Hp = (Hc - 1) / 2 + 1, Wp = (Wc - 1) / 2 + 1;  // 3x3/2/p1 pool output
   const int PWc = Wc + 3;
-  const int nranges = (Hp + STEM_ROWS_PER_WG - 1) / STEM_ROWS_PER_WG;
-  const int ri = blockIdx.x % nranges, zb = blockIdx.x / nranges;
-  const int b = zb % a.B, z = zb / a.B;
-  const int py0 = ri * STEM_ROWS_PER_WG, py1 = min(Hp, py0 + STEM_ROWS_PER_WG);
-  const int first = py0 > 0 ? -1 : 0;          // tile -1 computes conv rows 2*py0 - 2, 2*py0 - 1
-  const int ntiles = py1 - py0 - first;
+  const int npair = (Hp + 1) / 2;              // pooled-row pairs per image
+
+  // ---- this workgroup's model and run of (image, pair) steps
+  const int nwg = gridDim.x, base = nwg / a.Z, rem = nwg % a.Z, big = rem * (base + 1);
+  const int bx = blockIdx.x;
+  const int z = bx < big ? bx / (base + 1) : rem + (bx - big) / base;
+  const int gi = bx < big ? bx % (base + 1) : (bx - big) % base;
+  const int gsize = base + (z < rem ? 1 : 0);
+  const int T = a.B * npair;
+  const int j0 = (int)((int64_t)gi * T / gsize), j1 = (int)((int64_t)(gi + 1) * T / gsize);
+  if (j0 >= j1) return;  // uniform over the workgroup
+  const int carry = (j0 % npair) > 0 ? 1 : 0; // the first pair needs the conv rows above it
+  const int nsteps = j1 - j0 + carry;
+  // step s -> image and top conv row; pools unless it is the carry step
+  auto step_img = [&](int s) { return (j0 + max(s - carry, 0)) / npair; };
+  auto step_rho = [&](int s) {
+    const int j = j0 + max(s - carry, 0);
+    return STEM_TR * (j - (j / npair) * npair) - (s < carry ? STEM_TR : 0);
+  };
 
   const __amdgpu_buffer_rsrc_t rx = rsrc(reinterpret_cast<const uint16_t*>(a.x) + z * a.x_mstride,
                                          (uint32_t)((int64_t)a.B * a.H * a.W * 16 * 2));
@@ -570,11 +618,10 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
     const uint32_t off = (uint32_t)(((int64_t)n * a.Kp + ky * BK + lc * 8) * 2);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void*)(wsm + blk * 1024), 16, off, 0, 0, 0);
   }
-  // patch of the tile with top conv row rho0: input rows rho0 - 2 .. rho0 + 2,
-  // columns -2 .. Wc; 16-byte slot s = 2 * (pr * PWc + pc) + stored half
-  const int nslot = 5 * PWc * 2;
-  auto issue_patch = [&](int rho0, int buf) {
-    char* pb = psm + buf * STEM_PATCH;
+  // input rows rho0 - 2 .. rho0 + STEM_TR + 2, columns -2 .. Wc of image b;
+  // 16-byte slot s = 2 * (pr * PWc + pc) + stored half
+  const int nslot = STEM_PR * PWc * 2;
+  auto issue_patch = [&](int b, int rho0, char* pb) {
     for (int blk = wave; blk * 64 < nslot; blk += STEM_WAVES) {
       const int sl = blk * 64 + lane;
       uint32_t off = OOB;
@@ -589,10 +636,16 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
     }
   };
 
-  // this lane's pixel in the 2-row tile
-  const int pidx = wave * 32 + fr;
-  const bool pv = pidx < 2 * Wc;
-  const int pr0 = pv ? pidx / Wc : 0, pc0 = pv ? pidx - pr0 * Wc : 0;
+  // this lane's pixels: block i of the wave is step block wave * FM + i
+  int pr0[STEM_FM], pc0[STEM_FM];
+  bool pv[STEM_FM];
+#pragma unroll
+  for (int i = 0; i < STEM_FM; ++i) {
+    const int pidx = (wave * STEM_FM + i) * 32 + fr;
+    pv[i] = pidx < STEM_TR * Wc;
+    pr0[i] = pv[i] ? pidx / Wc : 0;
+    pc0[i] = pv[i] ? pidx - pr0[i] * Wc : 0;
+  }
   float bias_v[2][2][8];
   {
     const float* __restrict__ bias = a.bias + z * a.b_mstride;
@@ -603,82 +656,112 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) bias_v[j][h][e] = bias[j * 32 + 8 * (2 * h + fq) + e];
   }
-  uint16_t* __restrict__ y = reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride;
+  // pooled output through a buffer resource: every thread issues exactly
+  // STEM_NSTORE stores per pooling step (out-of-range ones are dropped), so
+  // the next step can wait for its input rows without waiting for them
+  constexpr int STEM_NSTORE = (2 * ((STEM_WMAX - 1) / 2 + 1) * 8 + 64 * STEM_WAVES - 1) / (64 * STEM_WAVES);
+  const __amdgpu_buffer_rsrc_t ry = rsrc(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride,
+                                         (uint32_t)((int64_t)a.B * Hp * Wp * 64 * 2));
 
-  issue_patch(2 * (py0 + first), 0);
-  for (int st = 0; st < ntiles; ++st) {
-    const int py = py0 + first + st, rho0 = 2 * py;
-    wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    if (st + 1 < ntiles) issue_patch(rho0 + 2, (st + 1) & 1);
-    const char* Pb = psm + (st & 1) * STEM_PATCH;
-    floatx16 acc[2];
+  auto do_step = [&](int st, const char* Pb, char* Pn) __attribute__((always_inline)) {
+    const int b = step_img(st), rho0 = step_rho(st);
+    wait_vmcnt<STEM_NSTORE>();  // this step's rows landed; the last step's stores may be in flight
+    wg_barrier();
+    if (st + 1 < nsteps) issue_patch(step_img(st + 1), step_rho(st + 1), Pn);
+    floatx16 acc[STEM_FM][2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int i = 0; i < STEM_FM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 #pragma unroll
     for (int ky = 0; ky < 4; ++ky) {
-      bf16x8 af[4], bfr[4][2];
 #pragma unroll
       for (int kx = 0; kx < 4; ++kx) {
-        const int pc = pc0 + kx;
-        const int slot = 2 * ((pr0 + ky) * PWc + pc) + (fq ^ ((pc >> 3) & 1));
-        af[kx] = *reinterpret_cast<const bf16x8*>(Pb + slot * 16);
+        bf16x8 af[STEM_FM], bfr[2];
+#pragma unroll
+        for (int i = 0; i < STEM_FM; ++i) {
+          const int pc = pc0[i] + kx;
+          const int slot = 2 * ((pr0[i] + ky) * PWc + pc) + (fq ^ ((pc >> 3) & 1));
+          af[i] = *reinterpret_cast<const bf16x8*>(Pb + slot * 16);
+        }
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           const int r = ky * 64 + j * 32 + fr;
-          bfr[kx][j] = *reinterpret_cast<const bf16x8*>(wsm + r * ROW + (((2 * kx + fq) ^ swz(r)) << 4));
+          bfr[j] = *reinterpret_cast<const bf16x8*>(wsm + r * ROW + (((2 * kx + fq) ^ swz(r)) << 4));
         }
+#pragma unroll
+        for (int i = 0; i < STEM_FM; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
       }
-#pragma unroll
-      for (int kx = 0; kx < 4; ++kx)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kx][j], af[kx], acc[j], 0, 0, 0);
     }
-    // activated bf16 conv rows into the LDS ring (row rho in buffer rho % 3)
-    const int rho = rho0 + pr0;
+    // activated bf16 conv rows into the LDS ring (row rho in buffer rho % 5)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int i = 0; i < STEM_FM; ++i) {
+      const int rho = rho0 + pr0[i];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int gp = 2 * h;
-        float v[8];
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[j][gp * 4 + r]),
-                                                           __float_as_uint(acc[j][(gp + 1) * 4 + r]), false, false);
-          v[r] = __uint_as_float(sw[0]);
-          v[4 + r] = __uint_as_float(sw[1]);
+        for (int h = 0; h < 2; ++h) {
+          const int gp = 2 * h;
+          float v[8];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
+                                                             __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
+            v[r] = __uint_as_float(sw[0]);
+            v[4 + r] = __uint_as_float(sw[1]);
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias_v[j][h][e], 0.f);
+          const int chunk = j * 4 + gp + fq;  // 8-channel group of the 64
+          if (pv[i] && rho >= 0 && rho < Hc)
+            *reinterpret_cast<uint4*>(rsm + (rho % STEM_RING) * RB + pc0[i] * ROW + ((chunk ^ swz(pc0[i])) << 4)) =
+                f8_to_bf8(v);
         }
+    }
+    const bool pool = st >= carry;  // the carry step only keeps the rows above the run
+    wait_lgkm0();
+    wg_barrier();
+    // pooled rows rho0/2 and rho0/2 + 1: conv rows 2py-1 .. 2py+1, columns 2px-1 .. 2px+1
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias_v[j][h][e], 0.f);
-        const int chunk = j * 4 + gp + fq;  // 8-channel group of the 64
-        if (pv && rho >= 0 && rho < Hc)
-          *reinterpret_cast<uint4*>(rsm + (rho % 3) * RB + pc0 * ROW + ((chunk ^ swz(pc0)) << 4)) = f8_to_bf8(v);
-      }
-    if (st == 0 && first < 0) continue;  // the row above the range only
-    __syncthreads();
-    // pooled row py: conv rows 2py-1 .. 2py+1, columns 2px-1 .. 2px+1
-    for (int item = tid; item < Wp * 8; item += 64 * STEM_WAVES) {
-      const int px = item >> 3, ch = item & 7;
+    for (int u = 0; u < STEM_NSTORE; ++u) {
+      const int item = tid + u * 64 * STEM_WAVES;
+      const int q = item / (Wp * 8), rest = item - q * (Wp * 8);
+      const int px = rest >> 3, ch = rest & 7;
+      const int py = rho0 / 2 + q;
+      const bool live = pool && q < 2 && py < Hp;
       float m[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
       for (int dy = -1; dy <= 1; ++dy) {
-        const int cr = rho0 + dy;
-        if (cr < 0 || cr >= Hc) continue;
+        const int cr = 2 * py + dy;
+        if (!live || cr < 0 || cr >= Hc) continue;
         for (int dx = -1; dx <= 1; ++dx) {
           const int cc = 2 * px + dx;
           if (cc < 0 || cc >= Wc) continue;
-          float q[8];
-          bf8_to_f8(*reinterpret_cast<const uint4*>(rsm + (cr % 3) * RB + cc * ROW + ((ch ^ swz(cc)) << 4)), q);
+          float qv[8];
+          bf8_to_f8(*reinterpret_cast<const uint4*>(rsm + (cr % STEM_RING) * RB + cc * ROW + ((ch ^ swz(cc)) << 4)), qv);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) m[e] = fmaxf(m[e], q[e]);
+          for (int e = 0; e < 8; ++e) m[e] = fmaxf(m[e], qv[e]);
         }
       }
-      *reinterpret_cast<uint4*>(y + (((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) = f8_to_bf8(m);
+      const uint32_t off = live ? (uint32_t)(((((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) * 2) : OOB;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(m)), ry, off, 0, 0);
     }
+  };
+
+  issue_patch(step_img(0), step_rho(0), psm0);
+  // STEM_NSTORE dropped stores, so that every step starts with the same count
+  // of stores in flight behind its rows
+#pragma unroll
+  for (int u = 0; u < STEM_NSTORE; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
+  for (int st = 0; st < nsteps; st += 2) {
+    do_step(st, psm0, psm1);
+    if (st + 1 < nsteps) do_step(st + 1, psm1, psm0);
   }
 }
 
@@ -797,8 +880,9 @@ bool conv_stem_pool_ok(const ConvArgs& a) { return stem_pool_ok_impl(a); }
 // y: the pooled [B][Hp][Wp][64] tensor; a.Ho x a.Wo is the conv output size.
 void launch_conv_stem_pool(const ConvArgs& a, hipStream_t s) {
   const int Hp = (a.Ho - 1) / 2 + 1;
-  const int nranges = (Hp + STEM_ROWS_PER_WG - 1) / STEM_ROWS_PER_WG;
-  hipLaunchKernelGGL(k_stem_pool, dim3(a.Z * a.B * nranges), dim3(64 * STEM_WAVES), 0, s, a);
+  const int steps = a.Z * a.B * ((Hp + 1) / 2);
+  const int nwg = std::max(a.Z, std::min(steps, cus_of_current_device()));
+  hipLaunchKernelGGL(k_stem_pool, dim3(nwg), dim3(64 * STEM_WAVES), 0, s, a);
 }
 
 void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s) {
