@@ -80,33 +80,47 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   }
 }
 
-// MFMAs of one 64-wide K-tile for a wave's FM x FN blocks of 32x32.
+// Operand fragments of half kh (k16 steps 2kh, 2kh+1) of a 64-wide K-tile.
 // ra[i] / rb[j]: the LDS row this lane supplies for A block i / B block j.
 // 32x32x16 operands: lane l supplies row (l & 31) of its block, k-group
-// (l >> 5) of 8; the weights are the A operand, so block (i, j) accumulates
-// D[n][m].
+// (l >> 5) of 8.
+template <int FM, int FN>
+__device__ __forceinline__ void frags_half(const char* As, const char* Bs, const int (&ra)[FM], const int (&rb)[FN],
+                                           int lane, int kh, bf16x8 (&af)[2][FM], bf16x8 (&bf)[2][FN]) {
+  const int fq = lane >> 5;
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int c = (kh * 2 + ks) * 2 + fq;  // logical 16-byte chunk
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8*>(As + ra[i] * ROW + ((c ^ swz(ra[i])) << 4));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bf[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + rb[j] * ROW + ((c ^ swz(rb[j])) << 4));
+  }
+}
+
+// MFMAs of one half K-tile; the weights are the A operand, so block (i, j)
+// accumulates D[n][m].
+template <int FM, int FN>
+__device__ __forceinline__ void mma_half(const bf16x8 (&af)[2][FM], const bf16x8 (&bf)[2][FN], floatx16 (&acc)[FM][FN]) {
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[ks][j], af[ks][i], acc[i][j], 0, 0, 0);
+}
+
+// MFMAs of one 64-wide K-tile for a wave's FM x FN blocks of 32x32; per
+// accumulator the k16 steps run 0, 1, 2, 3.
 template <int FM, int FN>
 __device__ __forceinline__ void mma_ktile_rows(const char* As, const char* Bs, const int (&ra)[FM],
                                                const int (&rb)[FN], int lane, floatx16 (&acc)[FM][FN]) {
-  const int fq = lane >> 5;
 #pragma unroll
-  for (int kh = 0; kh < 2; ++kh) {  // two halves of the 64-wide K-tile
+  for (int kh = 0; kh < 2; ++kh) {
     bf16x8 af[2][FM], bfr[2][FN];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int c = (kh * 2 + ks) * 2 + fq;  // logical 16-byte chunk
-#pragma unroll
-      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8*>(As + ra[i] * ROW + ((c ^ swz(ra[i])) << 4));
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + rb[j] * ROW + ((c ^ swz(rb[j])) << 4));
-    }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ks][j], af[ks][i], acc[i][j], 0, 0, 0);
+    frags_half<FM, FN>(As, Bs, ra, rb, lane, kh, af, bfr);
+    mma_half<FM, FN>(af, bfr, acc);
   }
 }
 
