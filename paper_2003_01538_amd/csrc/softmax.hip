@@ -100,9 +100,95 @@ __global__ void __launch_bounds__(SM_T) k_softmax_combine(SoftmaxArgs a) {
   }
 }
 
+// Up to 4 models of up to 1024 classes: the models of one image run side by
+// side, 256 threads (4 waves) each, with the same class-to-thread map and
+// the same reductions as above (so the same bits), and meet once in LDS for
+// the combination: S[c] = p_0[c] + p_1[c] + ... in model order.  The chain of
+// dependent steps is one model long instead of N.
+template <int NG>
+__global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a) {
+  constexpr int PER = 4, W = SM_T / 64;  // classes per thread, waves per model
+  __shared__ float ps[NG][PER * SM_T];
+  __shared__ float sv[NG * W];
+  __shared__ int si[NG * W];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int g = tid / SM_T, t = tid - g * SM_T, lane = tid & 63, wave = tid >> 6;
+  const bool live = g < a.N;
+  const float* row = a.logits + ((int64_t)(live ? g : 0) * a.B + b) * a.C;
+  float z[PER], best = -INFINITY;
+  int bi = a.C;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int c = t + j * SM_T;
+    z[j] = (live && c < a.C) ? row[c] : -INFINITY;
+    if (live && c < a.C && (z[j] > best || (z[j] == best && c < bi))) { best = z[j]; bi = c; }
+  }
+  wave_argmax(best, bi);
+  if (lane == 0) { sv[wave] = best; si[wave] = bi; }
+  __syncthreads();
+  best = sv[g * W]; bi = si[g * W];
+#pragma unroll
+  for (int w = 1; w < W; ++w)
+    if (sv[g * W + w] > best || (sv[g * W + w] == best && si[g * W + w] < bi)) { best = sv[g * W + w]; bi = si[g * W + w]; }
+  if (live && a.top1 && t == 0) a.top1[(int64_t)g * a.B + b] = bi;
+  float e[PER], part = 0.f;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    e[j] = (live && (t + j * SM_T) < a.C) ? expf(z[j] - best) : 0.f;
+    part += e[j];
+  }
+  part = wave_sum(part);
+  __syncthreads();  // every group has read its maxima
+  if (lane == 0) sv[wave] = part;
+  __syncthreads();
+  float d = 0.f;
+#pragma unroll
+  for (int w = 0; w < W; ++w) d += sv[g * W + w];
+  float* prow = a.probs + ((int64_t)(live ? g : 0) * a.B + b) * a.C;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int c = t + j * SM_T;
+    if (live && c < a.C) {
+      const float p = e[j] / d;
+      prow[c] = p;
+      ps[g][c] = p;
+    }
+  }
+  __syncthreads();
+  // combination over the classes, every thread of the block
+  float cb = -INFINITY;
+  int ci = a.C;
+  const float invn = (float)a.N;
+  for (int c = tid; c < a.C; c += SM_T * NG) {
+    float S = 0.f;
+    for (int m = 0; m < a.N; ++m) S += ps[m][c];
+    if (a.mean) a.mean[(int64_t)b * a.C + c] = S / invn;
+    if (S > cb || (S == cb && c < ci)) { cb = S; ci = c; }
+  }
+  wave_argmax(cb, ci);
+  __syncthreads();
+  if (lane == 0) { sv[wave] = cb; si[wave] = ci; }
+  __syncthreads();
+  if (tid == 0) {
+    float v = sv[0];
+    int i = si[0];
+    for (int w = 1; w < NG * W; ++w)
+      if (sv[w] > v || (sv[w] == v && si[w] < i)) { v = sv[w]; i = si[w]; }
+    a.vote[b] = i;
+  }
+}
+
 void launch_softmax_combine(const SoftmaxArgs& a, hipStream_t s) {
   const int per = (a.C + SM_T - 1) / SM_T;
   dim3 grid(a.B), block(SM_T);
+  if (per <= 4 && a.N <= 4) {
+    switch (a.N) {
+      case 1: hipLaunchKernelGGL(k_softmax_combine_mg<1>, grid, dim3(SM_T * 1), 0, s, a); return;
+      case 2: hipLaunchKernelGGL(k_softmax_combine_mg<2>, grid, dim3(SM_T * 2), 0, s, a); return;
+      case 3: hipLaunchKernelGGL(k_softmax_combine_mg<3>, grid, dim3(SM_T * 3), 0, s, a); return;
+      default: hipLaunchKernelGGL(k_softmax_combine_mg<4>, grid, dim3(SM_T * 4), 0, s, a); return;
+    }
+  }
   if (per <= 1) hipLaunchKernelGGL(k_softmax_combine<1>, grid, block, 0, s, a);
   else if (per <= 4) hipLaunchKernelGGL(k_softmax_combine<4>, grid, block, 0, s, a);
   else hipLaunchKernelGGL(k_softmax_combine<SM_PER>, grid, block, 0, s, a);
