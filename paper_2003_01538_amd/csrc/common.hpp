@@ -74,7 +74,12 @@ bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn);
 bool conv_stem_pool_ok(const ConvArgs& a);
 void launch_conv_stem_pool(const ConvArgs& a, hipStream_t s);
 void launch_conv_halo(const ConvArgs& a, int th, int tw, int bn, hipStream_t s);
-void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s);  // 1 or 2 launches (split-K reduce)
+void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s,
+                 bool reduce = true);  // 1 or 2 launches (split-K reduce unless !reduce)
+// Split-K completion fused with a following global average pool (bf16):
+// gy [Z][B][Cout] receives the pooled activations, which are not stored.
+bool conv_reduce_gap_ok(const ConvArgs& a);
+void launch_conv_splitk_reduce_gap(const ConvArgs& a, void* gy, int64_t gy_mstride, hipStream_t s);
 int conv_split(Prec p, const ConvArgs& a, int num_cus);
 size_t conv_partial_floats(const ConvArgs& a);
 void launch_conv_splitk_reduce(const ConvArgs& a, hipStream_t s);

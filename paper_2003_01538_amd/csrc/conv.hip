@@ -368,7 +368,7 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((k_conv<P, BM, BN, VEC, false>), dim3(tiles), dim3(NT), 0, s, a);
 }
 
-void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
+void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s, bool reduce) {
   if (p == BF16 && conv_tile(p, tile).halo) {
     const ConvTile& c = conv_tile(p, tile);
     launch_conv_halo(a, c.th, c.tw, c.bn, s);
@@ -377,7 +377,7 @@ void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s) {
   if (p == BF16 && conv_tile_direct(conv_tile(p, tile))) {
     const ConvTile& c = conv_tile(p, tile);
     launch_conv_dma(a, c.bm, c.bn, c.waves, c.wgm, c.dma, s);
-    if (a.split > 1) launch_conv_splitk_reduce(a, s);
+    if (a.split > 1 && reduce) launch_conv_splitk_reduce(a, s);
     return;
   }
   if (p == BF16) {

@@ -822,11 +822,87 @@ __global__ void __launch_bounds__(256) k_conv_splitk_reduce(ConvArgs a) {
   *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride + o) = f8_to_bf8(v);
 }
 
+// Split-K completion fused with the global average pool that is the conv's
+// only reader: a workgroup of 1024 threads owns one (model, image); thread (channel group
+// cg, pixel lane pl) finishes pixels pl, pl + PL, ... exactly as the plain
+// reduce does (partials in split order, bias, residual, ReLU, bf16 rounding:
+// the stored activation) and sums them in fp32; the PL lanes' sums are added
+// in lane order, divided by H*W and rounded once.  The activation tensor is
+// never written.  y: [B][Cout] per model.
+constexpr int RG_T = 1024;  // threads of the fused split-K completion + pool
+
+__global__ void __launch_bounds__(RG_T) k_conv_splitk_reduce_gap(ConvArgs a, uint16_t* gy, int64_t gy_mstride) {
+  __shared__ float part[RG_T][8];
+  const int CG = a.Cout / 8, PL = RG_T / CG;
+  const int z = blockIdx.x / a.B, b = blockIdx.x - z * a.B;
+  const int cg = threadIdx.x % CG, pl = threadIdx.x / CG, n = cg * 8;
+  const int HW = a.Ho * a.Wo;
+  const float* bias = a.bias + z * a.b_mstride + n;
+  float bv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bv[e] = bias[e];
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int p = pl; p < HW; p += PL) {
+    const int64_t m = (int64_t)b * HW + p;
+    float v[8];
+    const float4* p0 = reinterpret_cast<const float4*>(a.partial + ((int64_t)z * a.M + m) * a.Cout + n);
+    float4 q0 = p0[0], q1 = p0[1];
+    v[0] = q0.x; v[1] = q0.y; v[2] = q0.z; v[3] = q0.w; v[4] = q1.x; v[5] = q1.y; v[6] = q1.z; v[7] = q1.w;
+    for (int sp = 1; sp < a.split; ++sp) {
+      const float4* pp = reinterpret_cast<const float4*>(a.partial + (((int64_t)sp * a.Z + z) * a.M + m) * a.Cout + n);
+      q0 = pp[0]; q1 = pp[1];
+      v[0] += q0.x; v[1] += q0.y; v[2] += q0.z; v[3] += q0.w;
+      v[4] += q1.x; v[5] += q1.y; v[6] += q1.z; v[7] += q1.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] += bv[e];
+    if (a.res) {
+      float r[8];
+      bf8_to_f8(*reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride + m * a.Cout + n), r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += r[e];
+    }
+    if (a.relu)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+    float st[8];
+    bf8_to_f8(f8_to_bf8(v), st);  // the stored bf16 activation
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += st[e];
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[threadIdx.x][e] = acc[e];
+  __syncthreads();
+  if (pl != 0) return;
+  float t[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = part[cg][e];
+  for (int q = 1; q < PL; ++q)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[e] += part[q * CG + cg][e];
+  const float hw = (float)HW;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = t[e] / hw;
+  *reinterpret_cast<uint4*>(gy + z * gy_mstride + (int64_t)b * a.Cout + n) = f8_to_bf8(t);
+}
+
 }  // namespace
 
 void launch_conv_splitk_reduce(const ConvArgs& a, hipStream_t s) {
   const int64_t total = (int64_t)a.Z * a.M * (a.Cout / 8);
   hipLaunchKernelGGL(k_conv_splitk_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+}
+
+bool conv_reduce_gap_ok(const ConvArgs& a) {
+  const int cg = a.Cout / 8;
+  return a.split > 1 && a.Cout % 8 == 0 && cg >= 1 && cg <= RG_T && RG_T % cg == 0;
+}
+
+void launch_conv_splitk_reduce_gap(const ConvArgs& a, void* gy, int64_t gy_mstride, hipStream_t s) {
+  hipLaunchKernelGGL(k_conv_splitk_reduce_gap, dim3(a.Z * a.B), dim3(RG_T), 0, s, a, static_cast<uint16_t*>(gy),
+                     gy_mstride);
 }
 
 size_t conv_partial_floats(const ConvArgs& a) { return a.split > 1 ? (size_t)a.split * a.Z * a.M * a.Cout : 0; }

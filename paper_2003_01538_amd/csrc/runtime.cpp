@@ -119,6 +119,7 @@ struct LayerPlan {
   bool s2d = false;       // first conv rewritten on the space-to-depth input
   bool pool_fused = false;  // conv: also applies the next layer's 3x3/2 max pool, writes the pooled tensor
   bool fused_away = false;  // max pool: done by the conv before it (no launch, shares its slot)
+  bool gap_only = false;    // conv whose only reader is the global average pool right after it
   int kreal = 0;          // kh * kw * cin of the layer as specified (FLOP count)
   int in_c_real = 0;      // input channels as specified (byte count)
 };
@@ -420,6 +421,8 @@ void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
         } else if (L.src < 0) {
           e->need_plain = true;
         }
+        if (i + 2 < n && s.layers[i + 1].op == FS_OP_GAP && s.layers[i + 1].src == i && last_use[i] == i + 1)
+          P.gap_only = true;  // the split-K completion may also do the average pool
         if (P.s2d && L.relu && L.residual_src < 0 && L.cout == 64 && P.kh == 4 && P.pad == 2 && P.Kp == 256 &&
             P.out.W <= 112 && P.out.H == P.in.H && P.out.W == P.in.W && i + 1 < n - 1) {
           const fs_layer& Nx = s.layers[i + 1];  // a max pool that is the conv's only reader
@@ -737,8 +740,13 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
   const std::vector<std::vector<int>>& tiles = tiles_for(e, B, s);
   for (size_t gi = 0; gi < e->groups.size(); ++gi) {
     Group& g = e->groups[gi];
+    bool skip_next = false;  // the layer was done by the launch before it
     for (size_t li = 0; li < g.layers.size(); ++li) {
       LayerPlan& P = g.layers[li];
+      if (skip_next) {
+        skip_next = false;
+        continue;
+      }
       launch.group = (int)gi;
       launch.layer = (int)li;
       launch.Z = g.Z;
@@ -766,10 +774,21 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
                               (P.in_slot == SLOT_INPUT ? 1 : g.Z);
           const double out_px = P.pool_fused ? (double)B * ((P.out.H - 1) / 2 + 1) * ((P.out.W - 1) / 2 + 1) : a.M;
           const double bytes = in_b + ((double)a.Cout * kreal * esz + out_px * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
-          if (P.pool_fused)
+          if (P.pool_fused) {
             launch(K_CONV, flops, bytes, 1, [&] { launch_conv_stem_pool(a, s); });
-          else
+          } else if (P.gap_only && p == BF16 && conv_tile_direct(conv_tile(p, tile)) && conv_reduce_gap_ok(a)) {
+            // the split-K completion also takes the average pool of the next layer
+            const LayerPlan& G = g.layers[li + 1];
+            void* gy = slot_ptr(g, G.out_slot);
+            const int64_t gy_ms = (int64_t)g.slot_elems[G.out_slot] * Bm;
+            launch(K_CONV, flops, bytes, 2, [&] {
+              launch_conv(a, p, tile, s, false);
+              launch_conv_splitk_reduce_gap(a, gy, gy_ms, s);
+            });
+            skip_next = true;
+          } else {
             launch(K_CONV, flops, bytes, a.split > 1 ? 2 : 1, [&] { launch_conv(a, p, tile, s); });
+          }
           break;
         }
         case FS_OP_MAXPOOL:
@@ -826,15 +845,29 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
 
 int launches_per_pass(fs_ensemble* e) {
   int n = 1 + (e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0);  // preprocess + softmax/combine
-  for (Group& g : e->groups)
-    for (LayerPlan& P : g.layers) {
-      if (P.op == FS_OP_FC)
+  for (Group& g : e->groups) {
+    const std::vector<std::vector<int>>* tl = nullptr;
+    auto it = e->tiles.find(batch_bucket(e->max_batch, e->max_batch));
+    if (it != e->tiles.end()) tl = &it->second;
+    bool skip_next = false;
+    for (size_t li = 0; li < g.layers.size(); ++li) {
+      LayerPlan& P = g.layers[li];
+      if (skip_next) { skip_next = false; continue; }
+      if (P.op == FS_OP_FC) {
         n += fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus));
-      else if (P.op == FS_OP_CONV)
-        n += (!P.pool_fused && conv_args(e, g, P, e->max_batch, nullptr, 0).split > 1) ? 2 : 1;
-      else if (!P.fused_away)
+      } else if (P.op == FS_OP_CONV) {
+        const ConvArgs a = conv_args(e, g, P, e->max_batch, nullptr, 0);
+        n += (!P.pool_fused && a.split > 1) ? 2 : 1;
+        const int gi = (int)(&g - e->groups.data());
+        const int tile = tl ? (*tl)[gi][li] : conv_pick_tile(e->prec, a, e->num_cus);
+        if (P.gap_only && e->prec == BF16 && tile >= 0 && conv_tile_direct(conv_tile(e->prec, tile)) &&
+            conv_reduce_gap_ok(a))
+          skip_next = true;
+      } else if (!P.fused_away) {
         n += 1;
+      }
     }
+  }
   return n;
 }
 
