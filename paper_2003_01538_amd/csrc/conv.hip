@@ -280,7 +280,7 @@ __global__ void __launch_bounds__(NT, BM >= 256 ? 1 : 2) k_conv(ConvArgs a) {
       }
       if (a.relu)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+        for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
       *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
     } else {
       if (res) {
@@ -291,7 +291,7 @@ __global__ void __launch_bounds__(NT, BM >= 256 ? 1 : 2) k_conv(ConvArgs a) {
       }
       if (a.relu)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+        for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
       *reinterpret_cast<float4*>(y + o) = make_float4(v[0], v[1], v[2], v[3]);
       *reinterpret_cast<float4*>(y + o + 4) = make_float4(v[4], v[5], v[6], v[7]);
     }

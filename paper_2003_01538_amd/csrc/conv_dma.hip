@@ -188,7 +188,7 @@ __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&ac
         }
         if (a.relu)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+          for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
         *reinterpret_cast<uint4*>(y + o) = f8_to_bf8(v);
       }
     }
@@ -544,7 +544,7 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
             }
             if (a.relu)
 #pragma unroll
-              for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+              for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
             const int n = n0 + j * 32 + 8 * (gp + fq);
             const uint32_t off = mg[i] >= 0 ? (uint32_t)(((int64_t)mg[i] * a.Cout + n) * 2) : OOB;
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry, off, 0, 0);
@@ -558,29 +558,39 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
 // pad 2, on the [B][Hs][Ws][16] tensor, K = 256), bias, ReLU, bf16 rounding,
 // then the 3x3/2 max pool (pad 1), writing only the pooled tensor.  Rounding
 // before the max is exact: max commutes with a monotone rounding, so the
-// result equals the two layers run separately.
+// result equals the two layers run separately.  After the ReLU every value
+// is +0 or positive, whose bf16 bit patterns order like the values, so the
+// pool takes packed 16-bit integer maxima; window taps outside the image are
+// replaced by in-window neighbours (clamped), which leaves a max unchanged.
 //
 // Persistent: the workgroups are split evenly over the models, and each
 // walks a contiguous run of (image, pooled-row pair) steps of its model with
 // that model's 64 x 256 weights resident in LDS.  A step computes 4 conv rows
 // (2 pooled rows' worth) from the 7 input rows it needs, staged in LDS as
-// 32-byte pixels (the two 16-byte halves of pixel x are swapped when bit 3
-// of x is set, so the 16 consecutive pixels an operand read touches fall on
-// distinct banks) and double-buffered: the next step's rows load while this
-// step's MFMAs run.  Every 16-wide K step is one (Ky, Kx) tap, in the MFMA
-// order of the implicit GEMM.  The activated rows go to a ring of five LDS
-// row buffers (conv row r in buffer r % 5), from which the two pooled rows
-// are taken; the last conv row stays for the next pair.  A run that starts
+// 32-byte pixels at a fixed row stride (the two 16-byte halves of pixel x
+// are swapped when bit 3 of x is set, so the 16 consecutive pixels an
+// operand read touches fall on distinct banks) and double-buffered: the next
+// step's rows load while this step's MFMAs run.  Every 16-wide K step is one
+// (Ky, Kx) tap, in the MFMA order of the implicit GEMM.  The activated rows
+// go to a ring of five LDS row buffers (conv row r in buffer r % 5); the two
+// pooled rows of a step are taken from the ring while the next step's MFMAs
+// run, and the last conv row stays for the next pair.  A run that starts
 // below the top of an image first computes the four conv rows above it.
 // 7 waves, each two 32-pixel blocks x 64 channels (4 rows x 112 = 14 blocks).
 constexpr int STEM_WMAX = 112;                 // conv output width limit
-constexpr int STEM_PW = STEM_WMAX + 3;         // patch pixels per row
+constexpr int STEM_PW = STEM_WMAX + 3;         // patch pixels per row (fixed stride)
 constexpr int STEM_TR = 4;                     // conv rows per step
 constexpr int STEM_PR = STEM_TR + 3;           // input rows per step
 constexpr int STEM_RING = STEM_TR + 1;         // conv rows kept for pooling
-constexpr int STEM_PATCH = ((STEM_PR * STEM_PW * 32 + 1023) / 1024) * 1024;
+constexpr int STEM_NSLOT = STEM_PR * STEM_PW * 2;  // 16-byte patch slots
+constexpr int STEM_PATCH = ((STEM_NSLOT * 16 + 1023) / 1024) * 1024;
 constexpr int STEM_FM = 2;                     // 32-pixel blocks per wave
 constexpr int STEM_WAVES = (STEM_TR * STEM_WMAX + 32 * STEM_FM - 1) / (32 * STEM_FM);
+constexpr int STEM_PBLK = (STEM_NSLOT + 63) / 64;                           // patch load instructions
+constexpr int STEM_PIT = (STEM_PBLK + STEM_WAVES - 1) / STEM_WAVES;         // ... per wave
+constexpr int STEM_NSTORE = (2 * ((STEM_WMAX - 1) / 2 + 1) * 8 + 64 * STEM_WAVES - 1) / (64 * STEM_WAVES);
+
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
   constexpr int WB = 4 * 64 * ROW;             // resident weights
@@ -599,7 +609,6 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
   const int lr = lane >> 3, fr = lane & 31, fq = lane >> 5;
   const int Wc = a.Wo, Hc = a.Ho;              // conv output
   const int Hp = (Hc - 1) / 2 + 1, Wp = (Wc - 1) / 2 + 1;  // 3x3/2/p1 pool output
-  const int PWc = Wc + 3;
   const int npair = (Hp + 1) / 2;              // pooled-row pairs per image
 
   // ---- this workgroup's model and run of (image, pair) steps
@@ -632,26 +641,38 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
     const uint32_t off = (uint32_t)(((int64_t)n * a.Kp + ky * BK + lc * 8) * 2);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void*)(wsm + blk * 1024), 16, off, 0, 0, 0);
   }
-  // input rows rho0 - 2 .. rho0 + STEM_TR + 2, columns -2 .. Wc of image b;
-  // 16-byte slot s = 2 * (pr * PWc + pc) + stored half
-  const int nslot = STEM_PR * PWc * 2;
+  // patch of the step with top conv row rho0: input rows rho0 - 2 .. rho0 +
+  // STEM_TR + 2, columns -2 .. STEM_PW - 3; slot s = 2 * (pr * STEM_PW + pc) +
+  // stored half.  Per lane and load instruction the slot's row, column and
+  // byte offset within the pixel are fixed: precomputed.
+  int q_pr[STEM_PIT], q_ix[STEM_PIT], q_hb[STEM_PIT];
+#pragma unroll
+  for (int it = 0; it < STEM_PIT; ++it) {
+    const int sl = (it * STEM_WAVES + wave) * 64 + lane;
+    const int pix = sl >> 1, pr = pix / STEM_PW, pc = pix - pr * STEM_PW;
+    const bool ok = sl < STEM_NSLOT && pc - 2 < a.W;
+    q_pr[it] = ok ? pr - 2 : -(1 << 28);
+    q_ix[it] = pc - 2;
+    q_hb[it] = (((sl & 1) ^ ((pc >> 3) & 1)) * 8) * 2;
+  }
   auto issue_patch = [&](int b, int rho0, char* pb) {
-    for (int blk = wave; blk * 64 < nslot; blk += STEM_WAVES) {
-      const int sl = blk * 64 + lane;
-      uint32_t off = OOB;
-      if (sl < nslot) {
-        const int pix = sl >> 1, pr = pix / PWc, pc = pix - pr * PWc;
-        const int h = (sl & 1) ^ ((pc >> 3) & 1);
-        const int iy = rho0 - 2 + pr, ix = pc - 2;
-        if ((unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W)
-          off = (uint32_t)(((((int64_t)b * a.H + iy) * a.W + ix) * 16 + h * 8) * 2);
+    const int64_t img = (int64_t)b * a.H;
+#pragma unroll
+    for (int it = 0; it < STEM_PIT; ++it) {
+      const int blk = it * STEM_WAVES + wave;
+      if (blk < STEM_PBLK) {
+        const int iy = rho0 + q_pr[it], ix = q_ix[it];
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        const uint32_t off = ok ? (uint32_t)(((img + iy) * a.W + ix) * 32 + q_hb[it]) : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + blk * 1024), 16, off, 0, 0, 0);
       }
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + blk * 1024), 16, off, 0, 0, 0);
     }
   };
 
-  // this lane's pixels: block i of the wave is step block wave * FM + i
-  int pr0[STEM_FM], pc0[STEM_FM];
+  // ---- this lane's pixels (block i of the wave is step block wave * FM + i)
+  // and the byte offsets of its operands: A for (i, kx) at ky = 0 (the ky
+  // offset is a constant), B per kx (j and ky are constants)
+  int pr0[STEM_FM], pc0[STEM_FM], a_off[STEM_FM][4];
   bool pv[STEM_FM];
 #pragma unroll
   for (int i = 0; i < STEM_FM; ++i) {
@@ -659,7 +680,15 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
     pv[i] = pidx < STEM_TR * Wc;
     pr0[i] = pv[i] ? pidx / Wc : 0;
     pc0[i] = pv[i] ? pidx - pr0[i] * Wc : 0;
+#pragma unroll
+    for (int kx = 0; kx < 4; ++kx) {
+      const int pc = pc0[i] + kx;
+      a_off[i][kx] = (2 * (pr0[i] * STEM_PW + pc) + (fq ^ ((pc >> 3) & 1))) * 16;
+    }
   }
+  int b_off[4];
+#pragma unroll
+  for (int kx = 0; kx < 4; ++kx) b_off[kx] = fr * ROW + (((2 * kx + fq) ^ swz(fr)) << 4);
   float bias_v[2][2][8];
   {
     const float* __restrict__ bias = a.bias + z * a.b_mstride;
@@ -671,16 +700,45 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
         for (int e = 0; e < 8; ++e) bias_v[j][h][e] = bias[j * 32 + 8 * (2 * h + fq) + e];
   }
   // pooled output through a buffer resource: every thread issues exactly
-  // STEM_NSTORE stores per pooling step (out-of-range ones are dropped), so
-  // the next step can wait for its input rows without waiting for them
-  constexpr int STEM_NSTORE = (2 * ((STEM_WMAX - 1) / 2 + 1) * 8 + 64 * STEM_WAVES - 1) / (64 * STEM_WAVES);
+  // STEM_NSTORE stores per step (out-of-range ones are dropped), so the next
+  // step can wait for its input rows without waiting for them
   const __amdgpu_buffer_rsrc_t ry = rsrc(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride,
                                          (uint32_t)((int64_t)a.B * Hp * Wp * 64 * 2));
 
+  // the two pooled rows of step ps (whose activated rows are in the ring)
+  auto pool_step = [&](int ps, bool live_step) {
+    const int b = step_img(ps), rho0 = step_rho(ps);
+#pragma unroll
+    for (int u = 0; u < STEM_NSTORE; ++u) {
+      const int item = tid + u * 64 * STEM_WAVES;
+      const int q = item / (Wp * 8), rest = item - q * (Wp * 8);
+      const int px = rest >> 3, ch = rest & 7;
+      const int py = rho0 / 2 + q;
+      const bool live = live_step && q < 2 && py < Hp;
+      u16x8 m = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (live) {
+#pragma unroll
+        for (int dy = -1; dy <= 1; ++dy) {
+          const int cr = min(max(2 * py + dy, 0), Hc - 1);
+          const char* rowp = rsm + (cr % STEM_RING) * RB;
+#pragma unroll
+          for (int dx = -1; dx <= 1; ++dx) {
+            const int cc = min(max(2 * px + dx, 0), Wc - 1);
+            const uint4 v = *reinterpret_cast<const uint4*>(rowp + cc * ROW + ((ch ^ swz(cc)) << 4));
+            m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x8, v));
+          }
+        }
+      }
+      const uint32_t off = live ? (uint32_t)(((((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) * 2) : OOB;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, m), ry, off, 0, 0);
+    }
+  };
+
   auto do_step = [&](int st, const char* Pb, char* Pn) __attribute__((always_inline)) {
-    const int b = step_img(st), rho0 = step_rho(st);
+    const int rho0 = step_rho(st);
     wait_vmcnt<STEM_NSTORE>();  // this step's rows landed; the last step's stores may be in flight
-    wg_barrier();
+    wait_lgkm0();
+    wg_barrier();               // ...and every wave's activated rows of the last step are in the ring
     if (st + 1 < nsteps) issue_patch(step_img(st + 1), step_rho(st + 1), Pn);
     floatx16 acc[STEM_FM][2];
 #pragma unroll
@@ -695,16 +753,11 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
       for (int kx = 0; kx < 4; ++kx) {
         bf16x8 af[STEM_FM], bfr[2];
 #pragma unroll
-        for (int i = 0; i < STEM_FM; ++i) {
-          const int pc = pc0[i] + kx;
-          const int slot = 2 * ((pr0[i] + ky) * PWc + pc) + (fq ^ ((pc >> 3) & 1));
-          af[i] = *reinterpret_cast<const bf16x8*>(Pb + slot * 16);
-        }
+        for (int i = 0; i < STEM_FM; ++i)
+          af[i] = *reinterpret_cast<const bf16x8*>(Pb + a_off[i][kx] + ky * STEM_PW * 32);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int r = ky * 64 + j * 32 + fr;
-          bfr[j] = *reinterpret_cast<const bf16x8*>(wsm + r * ROW + (((2 * kx + fq) ^ swz(r)) << 4));
-        }
+        for (int j = 0; j < 2; ++j)
+          bfr[j] = *reinterpret_cast<const bf16x8*>(wsm + b_off[kx] + (ky * 64 + j * 32) * ROW);
 #pragma unroll
         for (int i = 0; i < STEM_FM; ++i)
 #pragma unroll
@@ -712,10 +765,16 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
       }
     }
+    // the previous step's pooled rows, while these MFMAs run
+    pool_step(st > 0 ? st - 1 : 0, st > 0 && st - 1 >= carry);
+    wait_lgkm0();
+    wg_barrier();  // the ring rows the pooling read may now be overwritten
     // activated bf16 conv rows into the LDS ring (row rho in buffer rho % 5)
 #pragma unroll
     for (int i = 0; i < STEM_FM; ++i) {
       const int rho = rho0 + pr0[i];
+      char* rowp = rsm + ((rho + STEM_RING) % STEM_RING) * RB + pc0[i] * ROW;
+      const int sw = swz(pc0[i]);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -724,47 +783,20 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
           float v[8];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
-                                                             __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
-            v[r] = __uint_as_float(sw[0]);
-            v[4 + r] = __uint_as_float(sw[1]);
+            const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
+                                                              __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
+            v[r] = __uint_as_float(sw2[0]);
+            v[4 + r] = __uint_as_float(sw2[1]);
           }
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias_v[j][h][e], 0.f);
+          for (int e = 0; e < 8; ++e) {
+            const float t = v[e] + bias_v[j][h][e];
+            v[e] = t > 0.f ? t : 0.f;  // +0 for every non-positive value
+          }
           const int chunk = j * 4 + gp + fq;  // 8-channel group of the 64
           if (pv[i] && rho >= 0 && rho < Hc)
-            *reinterpret_cast<uint4*>(rsm + (rho % STEM_RING) * RB + pc0[i] * ROW + ((chunk ^ swz(pc0[i])) << 4)) =
-                f8_to_bf8(v);
+            *reinterpret_cast<uint4*>(rowp + ((chunk ^ sw) << 4)) = f8_to_bf8(v);
         }
-    }
-    const bool pool = st >= carry;  // the carry step only keeps the rows above the run
-    wait_lgkm0();
-    wg_barrier();
-    // pooled rows rho0/2 and rho0/2 + 1: conv rows 2py-1 .. 2py+1, columns 2px-1 .. 2px+1
-#pragma unroll
-    for (int u = 0; u < STEM_NSTORE; ++u) {
-      const int item = tid + u * 64 * STEM_WAVES;
-      const int q = item / (Wp * 8), rest = item - q * (Wp * 8);
-      const int px = rest >> 3, ch = rest & 7;
-      const int py = rho0 / 2 + q;
-      const bool live = pool && q < 2 && py < Hp;
-      float m[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
-      for (int dy = -1; dy <= 1; ++dy) {
-        const int cr = 2 * py + dy;
-        if (!live || cr < 0 || cr >= Hc) continue;
-        for (int dx = -1; dx <= 1; ++dx) {
-          const int cc = 2 * px + dx;
-          if (cc < 0 || cc >= Wc) continue;
-          float qv[8];
-          bf8_to_f8(*reinterpret_cast<const uint4*>(rsm + (cr % STEM_RING) * RB + cc * ROW + ((ch ^ swz(cc)) << 4)), qv);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) m[e] = fmaxf(m[e], qv[e]);
-        }
-      }
-      const uint32_t off = live ? (uint32_t)(((((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) * 2) : OOB;
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(m)), ry, off, 0, 0);
     }
   };
 
@@ -777,6 +809,9 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
     do_step(st, psm0, psm1);
     if (st + 1 < nsteps) do_step(st + 1, psm1, psm0);
   }
+  wait_lgkm0();
+  wg_barrier();
+  pool_step(nsteps - 1, nsteps - 1 >= carry);
 }
 
 bool stem_pool_ok_impl(const ConvArgs& a) {
@@ -818,7 +853,7 @@ __global__ void __launch_bounds__(256) k_conv_splitk_reduce(ConvArgs a) {
   }
   if (a.relu)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+    for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
   *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride + o) = f8_to_bf8(v);
 }
 
@@ -866,7 +901,7 @@ __global__ void __launch_bounds__(RG_T) k_conv_splitk_reduce_gap(ConvArgs a, uin
     }
     if (a.relu)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.f);
+      for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
     float st[8];
     bf8_to_f8(f8_to_bf8(v), st);  // the stored bf16 activation
 #pragma unroll

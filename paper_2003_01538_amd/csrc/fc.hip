@@ -127,7 +127,7 @@ __global__ void __launch_bounds__(256) k_fc(FcArgs a) {
         a.partial[(((int64_t)sp * a.Z + model) * a.B + bb) * a.N + n] = acc[f][r];
       } else {
         float v = acc[f][r] + bias[n];
-        if (a.relu) v = fmaxf(v, 0.f);
+        if (a.relu) v = v > 0.f ? v : 0.f;
         const int64_t o = (int64_t)bb * a.N + n;
         if (a.out_f32 || P == F32)
           (reinterpret_cast<float*>(a.y) + model * a.y_mstride)[o] = v;
@@ -150,7 +150,7 @@ __global__ void __launch_bounds__(256) k_fc_reduce(FcArgs a, int out_bf16) {
   for (int sp = 0; sp < a.split; ++sp)
     v += a.partial[(((int64_t)sp * a.Z + model) * a.B + bb) * a.N + n];
   v += a.bias[model * a.b_mstride + n];
-  if (a.relu) v = fmaxf(v, 0.f);
+  if (a.relu) v = v > 0.f ? v : 0.f;
   const int64_t o = (int64_t)bb * a.N + n;
   if (out_bf16)
     (reinterpret_cast<uint16_t*>(a.y) + model * a.y_mstride)[o] = f2bf(v);
