@@ -52,23 +52,29 @@ struct ConvTile {
   int dma = 0;       // 0: register-staged gather kernel; >0: LDS-DMA kernel with this many stages
   int waves = 4;     // LDS-DMA kernel: waves per workgroup
   int wgm = 2;       // LDS-DMA kernel: waves along M
-  int halo = 0;      // 1: direct 3x3 kernel with the input halo in LDS,
-  int th = 0, tw = 0;  //    tiles of th output rows x tw (= output width) columns
+  int halo = 0;      // 1: direct 3x3 kernel with the input halo and the weights in LDS,
+  int th = 0, tw = 0;  //    tiles of th output rows x tw (= output width) columns;
+                       // 2: direct 3x3 kernel, input halo in LDS, weights streamed per tap
 };
 // Every LDS-DMA tile shares one MFMA step and K order, so all of them
 // produce bit-identical sums.
 inline bool conv_tile_direct(const ConvTile& c) { return c.dma > 0; }
-// Kernel family of a tile: 2 halo, 1 LDS-DMA implicit GEMM, 0 register-staged
-// implicit GEMM.  A layer always runs in the highest family that fits it, and
-// tiles are only ever compared within one family.
-inline int conv_tile_family(const ConvTile& c) { return c.halo ? 2 : (c.dma > 0 ? 1 : 0); }
+// Kernel family of a tile: 3 halo with streamed weights, 2 halo with resident
+// weights, 1 LDS-DMA implicit GEMM, 0 register-staged implicit GEMM.  A layer
+// always runs in the highest family that fits it, and tiles are only ever
+// compared within one family.
+inline int conv_tile_family(const ConvTile& c) { return c.halo == 2 ? 3 : c.halo ? 2 : (c.dma > 0 ? 1 : 0); }
 int conv_num_tiles(Prec p);
 const ConvTile& conv_tile(Prec p, int t);
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);
-bool conv_tile_ok(Prec p, int t, const ConvArgs& a);
+bool conv_tile_ok(Prec p, int t, const ConvArgs& a);         // the tile's kernel can run the layer
+bool conv_tile_candidate(Prec p, int t, const ConvArgs& a);  // ... and is among its automatic choices
 bool conv_dma_ok(const ConvArgs& a);
 void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s);
 bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn);
+bool conv_hs_ok(const ConvArgs& a);      // the streamed-weight halo kernel can run the layer
+bool conv_hs_chosen(const ConvArgs& a);  // ... and is its automatic choice
+void launch_conv_hs(const ConvArgs& a, hipStream_t s);
 // Space-to-depth ResNet stem (4x4/1/p2 on 16 channels, 64 outputs, ReLU)
 // fused with the following 3x3/2/p1 max pool; y receives the pooled tensor.
 bool conv_stem_pool_ok(const ConvArgs& a);

@@ -316,6 +316,7 @@ static const ConvTile kTilesBF16[] = {
     {64, 128, 8, "bf16dma2_64x128_w4_v8", 2, 4, 2},
     {256, 64, 8, "bf16dma2_256x64_w4m4_v8", 2, 4, 4},
     {224, 64, 8, "bf16halo_4x56_n64_v8", 0, 7, 7, 1, 4, 56},
+    {128, 128, 8, "bf16hs_128x128_w4_v8", 0, 4, 2, 2},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -331,10 +332,18 @@ const ConvTile& conv_tile(Prec p, int t) { return p == BF16 ? kTilesBF16[t] : kT
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (t < 0 || t >= conv_num_tiles(p)) return false;
   const ConvTile& c = conv_tile(p, t);
+  if (c.halo == 2) return p == BF16 && conv_hs_ok(a);
   if (c.halo) return p == BF16 && conv_halo_ok(a, c.th, c.tw, c.bn);
   if (conv_tile_direct(c)) return p == BF16 && conv_dma_ok(a);
   if (a.split > 1) return false;  // only the LDS-DMA kernels split K
   return a.Cin % c.vec == 0 && a.Kp % CONV_KPAD == 0 && a.Cout % 8 == 0;
+}
+
+// Whether tile t is among the layer's automatic choices (see conv_hs_chosen
+// for the streamed-weight halo kernel).
+bool conv_tile_candidate(Prec p, int t, const ConvArgs& a) {
+  if (!conv_tile_ok(p, t, a)) return false;
+  return conv_tile(p, t).halo != 2 || conv_hs_chosen(a);
 }
 
 // Largest useful tile: prefer tiles that keep >= 2 workgroups per CU busy,
@@ -342,11 +351,11 @@ bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus) {
   int fam = -1;
   for (int t = 0; t < conv_num_tiles(p); ++t)
-    if (conv_tile_ok(p, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(p, t)));
+    if (conv_tile_candidate(p, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(p, t)));
   int best = -1;
   double best_score = -1;
   for (int t = 0; t < conv_num_tiles(p); ++t) {
-    if (!conv_tile_ok(p, t, a) || conv_tile_family(conv_tile(p, t)) != fam) continue;
+    if (!conv_tile_candidate(p, t, a) || conv_tile_family(conv_tile(p, t)) != fam) continue;
     const ConvTile& c = conv_tile(p, t);
     const double tm = (a.M + c.bm - 1) / c.bm, tn = (a.Cout + c.bn - 1) / c.bn;
     const double wgs = tm * tn * a.Z;
@@ -369,6 +378,10 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
 }
 
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s, bool reduce) {
+  if (p == BF16 && conv_tile(p, tile).halo == 2) {
+    launch_conv_hs(a, s);
+    return;
+  }
   if (p == BF16 && conv_tile(p, tile).halo) {
     const ConvTile& c = conv_tile(p, tile);
     launch_conv_halo(a, c.th, c.tw, c.bn, s);

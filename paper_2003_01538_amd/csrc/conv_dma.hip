@@ -30,43 +30,13 @@
 // models of a group.
 #include "common.hpp"
 #include "device.hpp"
+#include "lds_dma.hpp"
 
 #include <algorithm>
 
 namespace fs {
 
 namespace {
-
-typedef __attribute__((address_space(3))) void lds_void;
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-
-constexpr int BK = 64;          // bf16 elements per K-tile row (128 bytes)
-constexpr int ROW = 128;        // LDS bytes per tile row
-constexpr uint32_t OOB = 0x80000000u;
-
-__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-
-// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// s_waitcnt lgkmcnt(0), leaving vmcnt and expcnt alone
-__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4)); }
-
-// Workgroup barrier without a memory fence (so it does not wait for vector
-// memory operations); the compiler may not move memory accesses across it.
-__device__ __forceinline__ void wg_barrier() {
-  __asm__ __volatile__("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  __asm__ __volatile__("" ::: "memory");
-}
 
 // Wait until at most `ahead` K-tiles (LPT load instructions each) of this
 // wave are still in flight; `ahead` <= A (vmcnt takes an immediate).
@@ -947,7 +917,7 @@ size_t conv_partial_floats(const ConvArgs& a) { return a.split > 1 ? (size_t)a.s
 // layer has fewer than three 64x64 output tiles per CU, keeping >= 8 K-tiles
 // per split.
 int conv_split(Prec p, const ConvArgs& a, int num_cus) {
-  if (p != BF16 || !conv_dma_ok(a)) return 1;
+  if (p != BF16 || !conv_dma_ok(a) || conv_hs_chosen(a)) return 1;  // the streamed-weight halo kernel never splits
   const int64_t units = (int64_t)((a.M + 63) / 64) * ((a.Cout + 63) / 64) * a.Z;
   const int nk = a.Kp / BK;
   int split = 1;

@@ -681,14 +681,14 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
         e->workspace_bytes += (int64_t)e->conv_partial.bytes;
         a.partial = static_cast<float*>(e->conv_partial.p);
       }
-      int fam = -1;  // the layer runs in the highest kernel family that fits it
+      int fam = -1;  // the layer runs in the highest kernel family among its candidates
       for (int t = 0; t < conv_num_tiles(e->prec); ++t)
-        if (conv_tile_ok(e->prec, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(e->prec, t)));
+        if (conv_tile_candidate(e->prec, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(e->prec, t)));
       int best = conv_pick_tile(e->prec, a, e->num_cus);
       if (e->tune) {
         float best_ms = 1e30f;
         for (int t = 0; t < conv_num_tiles(e->prec); ++t) {
-          if (!conv_tile_ok(e->prec, t, a) || conv_tile_family(conv_tile(e->prec, t)) != fam) continue;
+          if (!conv_tile_candidate(e->prec, t, a) || conv_tile_family(conv_tile(e->prec, t)) != fam) continue;
           launch_conv(a, e->prec, t, s);
           HIPCHK(hipEventRecord(e0, s));
           launch_conv(a, e->prec, t, s);

@@ -94,7 +94,15 @@ CONV_CASES = [
     (1, 5, 6, 16, 32, 3, 1, 1, 1, 0),      # tiny-net second conv
     (2, 12, 56, 64, 64, 3, 1, 1, 1, 1),    # halo kernel, 4-row tiles of width 56
     (3, 10, 56, 64, 64, 3, 1, 1, 0, 0),    # halo kernel, partial last row tile, no residual / ReLU
+    (2, 12, 20, 128, 128, 3, 1, 1, 1, 1),  # streamed-weight halo: tiles across rows and images, ragged M
+    (3, 10, 9, 128, 256, 3, 1, 1, 0, 0),   # streamed-weight halo: two channel tiles, no residual / ReLU
+    (1, 1, 1, 128, 128, 3, 1, 1, 1, 1),    # 1x1 image: every tap but the centre is padding
+    (3, 2, 23, 128, 128, 3, 1, 1, 1, 0),   # streamed-weight halo, 40-block patch, tiles across images
+    (1, 4, 70, 128, 128, 3, 1, 1, 1, 1),   # streamed-weight halo with its largest patch (48 blocks)
+    (2, 5, 70, 128, 128, 3, 1, 1, 1, 0),   # patch too large for it: the implicit GEMM takes the layer
 ]
+# cases the streamed-weight halo kernel (3x3/1, Cin and Cout multiples of 128) fits
+HS_CASES = (5, 10, 11, 12, 13, 14)
 
 
 def _conv_inputs(case, prec, seed):
@@ -149,6 +157,8 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
         assert ran >= 2 + sum(1 for t in tiles if "dma" in fsb.fs_conv_tile_name(prec, t))
     if prec == BF16 and k == 3 and s == 1 and Cin == 64 and Cout % 64 == 0 and W == 56:  # and the halo kernel
         assert any("halo" in n for n in ran_names), ran_names
+    if prec == BF16:  # the streamed-weight halo kernel exactly where it fits
+        assert any("hs_" in n for n in ran_names) == (ci in HS_CASES), ran_names
 
 
 def _tile_index(name_part):
@@ -158,7 +168,7 @@ def _tile_index(name_part):
 def test_halo_kernel_bits_equal_implicit_gemm_for_one_chunk(gpu_lib):
     # With Cin = 64 the halo kernel sums each output over the taps in the
     # implicit GEMM's K order with the same MFMA sequence: identical bits.
-    x, w, b, r = _conv_inputs(CONV_CASES[-2], BF16, 17)  # 12 x 56, Cin 64, residual
+    x, w, b, r = _conv_inputs(CONV_CASES[8], BF16, 17)  # 12 x 56, Cin 64, residual
     g_halo = fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16, tile=_tile_index("halo_4x56"))
     g_dma = fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16, tile=_tile_index("dma2_128x64"))
     assert np.array_equal(g_halo.view(np.uint32), g_dma.view(np.uint32))
