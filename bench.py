@@ -52,7 +52,7 @@ PROFILE = os.path.join(ROOT, "profiles", "conv_resnet18x3_b32.md")
 def conv_source_hash():
     import hashlib
     h = hashlib.sha256()
-    for f in ("conv.hip", "conv_dma.hip"):
+    for f in ("conv.hip", "conv_dma.hip", "conv_hs.hip", "lds_dma.hpp"):
         with open(os.path.join(ROOT, "paper_2003_01538_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -81,6 +81,27 @@ __device__ __forceinline__ void mma_half(const bf16x8 (&af)[2][FM], const bf16x8
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[ks][j], af[ks][i], acc[i][j], 0, 0, 0);
 }
 
+// The same with the A rows' swizzles given (sa[i] instead of swz(ra[i])).
+template <int FM, int FN>
+__device__ __forceinline__ void mma_ktile_rows_sw(const char* As, const char* Bs, const int (&ra)[FM],
+                                                  const int (&sa)[FM], const int (&rb)[FN], int lane,
+                                                  floatx16 (&acc)[FM][FN]) {
+  const int fq = lane >> 5;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh) {
+    bf16x8 af[2][FM], bfr[2][FN];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = (kh * 2 + ks) * 2 + fq;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8*>(As + ra[i] * ROW + ((c ^ sa[i]) << 4));
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + rb[j] * ROW + ((c ^ swz(rb[j])) << 4));
+    }
+    mma_half<FM, FN>(af, bfr, acc);
+  }
+}
+
 // MFMAs of one 64-wide K-tile for a wave's FM x FN blocks of 32x32; per
 // accumulator the k16 steps run 0, 1, 2, 3.
 template <int FM, int FN>
@@ -318,7 +339,11 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
 // starts, so neither waits at the epilogue.  Per output, the sum runs over
 // chunks, then taps, then the 64 channels in the same MFMA order as the
 // implicit GEMM; with one chunk (Cin = 64) the order, and so every bit, is
-// that of the implicit GEMM.
+// that of the implicit GEMM.  Patch pixel (r, c) (patch row, padded column)
+// is swizzled by h = r * TW + c, which runs consecutively over the 16
+// outputs an operand read serves per cycle, also across an output row's end
+// (where the patch index skips the two padding columns), so the reads are
+// free of bank conflicts at every tap.
 template <int TH, int TW, int BN, int FM, int WBYTES>
 __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvArgs a) {
   constexpr int P = TH * TW, MB = P / 32, NW = MB / FM, FN = BN / 32;
@@ -371,7 +396,7 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
   for (int it = 0; it < NIT; ++it) {
     const int blk = it * NW + wave;
     const int q = blk * 8 + lr;
-    q_lc[it] = (lane & 7) ^ swz(q);
+    q_lc[it] = (lane & 7) ^ (((q / PW * TW + q % PW) >> 1) & 7);
     if (blk < NPB && q < NP) {
       const int pr = q / PW;
       q_dy[it] = pr - 1;
@@ -400,13 +425,14 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
   // ---- this lane's pixels (block i of the wave is tile block wave * FM + i)
   // and, for the epilogue, its 8-channel groups: after the permlane32 swap a
   // lane holds channels n0 + 32 j + 8 (gp + fq) .. +8 of its pixel, gp = 0, 2
-  int q0[FM], pr_[FM], pc_[FM];
+  int q0[FM], h0[FM], pr_[FM], pc_[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int pidx = (wave * FM + i) * 32 + fr;
     pr_[i] = pidx / TW;
     pc_[i] = pidx - pr_[i] * TW;
     q0[i] = pr_[i] * PW + pc_[i];
+    h0[i] = pr_[i] * TW + pc_[i];
   }
   float bias_v[FN][2][8];
   {
@@ -479,12 +505,15 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
     for (int tap = 0; tap < 9; ++tap) {
       const int ky = tap / 3, kx = tap - ky * 3;
       const int kt = tap * CH + cc;
-      int ra[FM], rb[FN];
+      int ra[FM], sa[FM], rb[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) ra[i] = q0[i] + ky * PW + kx;
+      for (int i = 0; i < FM; ++i) {
+        ra[i] = q0[i] + ky * PW + kx;
+        sa[i] = ((h0[i] + ky * TW + kx) >> 1) & 7;
+      }
 #pragma unroll
       for (int j = 0; j < FN; ++j) rb[j] = kt * BN + j * 32 + fr;
-      mma_ktile_rows<FM, FN>(Pb, wsm, ra, rb, lane, acc);
+      mma_ktile_rows_sw<FM, FN>(Pb, wsm, ra, sa, rb, lane, acc);
     }
     if (cc != CH - 1) {
 #pragma unroll
