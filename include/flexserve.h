@@ -133,6 +133,15 @@ fs_status fs_infer_device(fs_ensemble *e, const uint8_t *d_pixels,
                           float *d_probs, float *d_mean_probs, int32_t *d_vote,
                           int32_t *d_top1, float *d_logits, void *stream);
 
+/* HIP graphs for the pass (on by default).  fs_infer and fs_infer_device
+ * record the pass's kernel launches the first time a batch size meets a set
+ * of buffers on a stream and replay them with one launch from then on
+ * (the scheduler row of the hot path: one graph per exact batch size).  The
+ * pass runs eagerly while the profiler is on and on the legacy default
+ * stream.  enable = 0 turns graphs off and drops the recorded passes.
+ * Synchronises the ensemble's stream.  FS_ERR_INVALID for a NULL handle. */
+fs_status fs_graphs_enable(fs_ensemble *e, int32_t enable);
+
 void fs_destroy(fs_ensemble *e); /* NULL-safe; waits for outstanding work */
 
 /* Last error message of handle e, or of this thread's last failed create

@@ -169,6 +169,10 @@ struct fs_ensemble {
   // conv tile per (batch bucket) -> per group -> per layer, measured once
   std::map<int, std::vector<std::vector<int>>> tiles;
   bool tune = true;
+  // captured passes, replayed with one launch: key = batch size, stream and
+  // every buffer the pass reads or writes (caller's and the ensemble's own)
+  bool graphs = true;
+  std::map<std::vector<uintptr_t>, hipGraphExec_t> graph_cache;
   // profiler
   bool prof_on = false;
   std::vector<ProfRec> prof;
@@ -893,10 +897,61 @@ fs_status guarded(fs_ensemble* e, F&& fn) {
   }
 }
 
+void clear_graphs(fs_ensemble* e) {
+  for (auto& kv : e->graph_cache) (void)hipGraphExecDestroy(kv.second);
+  e->graph_cache.clear();
+}
+
+// One pass.  With graphs on (and the profiler off), the pass is captured the
+// first time this exact batch size meets these buffers on this stream and
+// replayed from then on; the tile plan of the batch bucket (which may time
+// candidates and grow the split-K scratch) is made before the capture, so
+// only kernel launches are recorded.  A capture that fails turns graphs off
+// for the ensemble and the pass runs eagerly.
+void run_pass_cached(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
+                     float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s) {
+  if (!e->graphs || e->prof_on || s == nullptr) {
+    run_pass(e, d_pixels, d_desc, B, d_probs, d_mean, d_vote, d_top1, d_logits, s);
+    return;
+  }
+  tiles_for(e, B, s);
+  const std::vector<uintptr_t> key = {
+      (uintptr_t)B, (uintptr_t)s, (uintptr_t)d_pixels, (uintptr_t)d_desc, (uintptr_t)d_probs, (uintptr_t)d_mean,
+      (uintptr_t)d_vote, (uintptr_t)d_top1, (uintptr_t)d_logits, (uintptr_t)e->logits.p,
+      (uintptr_t)e->conv_partial.p, (uintptr_t)e->partial.p};
+  auto it = e->graph_cache.find(key);
+  if (it == e->graph_cache.end()) {
+    if (e->graph_cache.size() >= 64) clear_graphs(e);
+    hipGraph_t g = nullptr;
+    hipGraphExec_t x = nullptr;
+    bool ok = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) == hipSuccess;
+    if (ok) {
+      try {
+        run_pass(e, d_pixels, d_desc, B, d_probs, d_mean, d_vote, d_top1, d_logits, s);
+      } catch (...) {
+        if (hipStreamEndCapture(s, &g) == hipSuccess && g) (void)hipGraphDestroy(g);
+        throw;
+      }
+      ok = hipStreamEndCapture(s, &g) == hipSuccess && g;
+      ok = ok && hipGraphInstantiate(&x, g, nullptr, nullptr, 0) == hipSuccess;
+      if (g) (void)hipGraphDestroy(g);
+    }
+    if (!ok) {
+      (void)hipGetLastError();
+      e->graphs = false;
+      run_pass(e, d_pixels, d_desc, B, d_probs, d_mean, d_vote, d_top1, d_logits, s);
+      return;
+    }
+    it = e->graph_cache.emplace(key, x).first;
+  }
+  HIPCHK(hipGraphLaunch(it->second, s));
+}
+
 void destroy_impl(fs_ensemble* e) {
   if (!e) return;
   if (hipSetDevice(e->device) == hipSuccess) {
     if (e->stream) (void)hipStreamSynchronize(e->stream);
+    clear_graphs(e);
     prof_clear(e);
     for (hipEvent_t ev : e->ev_pool) (void)hipEventDestroy(ev);
     e->ev_pool.clear();
@@ -1013,8 +1068,8 @@ fs_status fs_infer_device(fs_ensemble* e, const uint8_t* d_pixels, const fs_imag
     if (!d_pixels || !d_desc || !d_probs || !d_vote) fail(FS_ERR_INVALID, "required device pointer is NULL");
     HIPCHK(hipSetDevice(e->device));
     hipStream_t s = stream ? static_cast<hipStream_t>(stream) : e->stream;
-    run_pass(e, d_pixels, reinterpret_cast<const ImageDesc*>(d_desc), B, d_probs, d_mean_probs, d_vote,
-             d_top1, d_logits, s);
+    run_pass_cached(e, d_pixels, reinterpret_cast<const ImageDesc*>(d_desc), B, d_probs, d_mean_probs, d_vote,
+                    d_top1, d_logits, s);
   });
 }
 
@@ -1050,9 +1105,9 @@ fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs
       HIPCHK(hipMemcpyAsync(e->d_pixels.p, e->h_pixels.p, pbytes, hipMemcpyHostToDevice, s));
       HIPCHK(hipMemcpyAsync(e->d_desc.p, hd, nb * sizeof(ImageDesc), hipMemcpyHostToDevice, s));
       float* dlog = static_cast<float*>(e->logits.p);
-      run_pass(e, static_cast<const uint8_t*>(e->d_pixels.p), static_cast<const ImageDesc*>(e->d_desc.p), nb,
-               static_cast<float*>(e->d_probs.p), mean_probs ? static_cast<float*>(e->d_mean.p) : nullptr,
-               static_cast<int32_t*>(e->d_vote.p), static_cast<int32_t*>(e->d_top1.p), dlog, s);
+      run_pass_cached(e, static_cast<const uint8_t*>(e->d_pixels.p), static_cast<const ImageDesc*>(e->d_desc.p),
+                      nb, static_cast<float*>(e->d_probs.p), mean_probs ? static_cast<float*>(e->d_mean.p) : nullptr,
+                      static_cast<int32_t*>(e->d_vote.p), static_cast<int32_t*>(e->d_top1.p), dlog, s);
       float* hp = static_cast<float*>(e->h_out.p);
       float* hl = hp + (size_t)N * Bm * C;
       float* hm = hl + (size_t)N * Bm * C;
@@ -1102,6 +1157,20 @@ fs_status fs_query(const fs_ensemble* ce, fs_info* info) {
     info->weight_bytes = (int64_t)e->arena_bytes;
     info->workspace_bytes = e->workspace_bytes;
     info->flops_per_image = e->flops_per_image;
+  });
+}
+
+fs_status fs_graphs_enable(fs_ensemble* e, int32_t enable) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    HIPCHK(hipSetDevice(e->device));
+    HIPCHK(hipStreamSynchronize(e->stream));
+    clear_graphs(e);
+    e->graphs = enable != 0;
   });
 }
 

@@ -97,6 +97,7 @@ SIGNATURES = [
     ("fs_last_error", ctypes.c_char_p, [_vp]),
     ("fs_query", ctypes.c_int, [_vp, ctypes.POINTER(fs_info)]),
     ("fs_profile_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
+    ("fs_graphs_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
     ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
@@ -268,6 +269,10 @@ def fs_query(handle) -> dict:
     info = fs_info()
     _check(load().fs_query(handle, ctypes.byref(info)), handle)
     return {k: getattr(info, k) for k, _ in fs_info._fields_}
+
+
+def fs_graphs_enable(handle, enable=True):
+    _check(load().fs_graphs_enable(handle, int(bool(enable))), handle)
 
 
 def fs_profile_enable(handle, enable=True):

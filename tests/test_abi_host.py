@@ -107,6 +107,7 @@ def test_calls_on_null_handle_fail_cleanly():
     assert lib.fs_infer_device(None, None, None, 1, None, None, None, None, None, None) == fsb.FS_ERR_INVALID
     assert lib.fs_query(None, None) == fsb.FS_ERR_INVALID
     assert lib.fs_profile_enable(None, 1) == fsb.FS_ERR_INVALID
+    assert lib.fs_graphs_enable(None, 1) == fsb.FS_ERR_INVALID
     lib.fs_destroy(None)
 
 

@@ -166,3 +166,29 @@ def test_profiler_counts_every_launch():
         # 20 conv layers; a layer whose reduction is split over workgroups adds a reduce launch
         assert 20 <= st["conv"]["launches"] <= 40 and st["conv"]["total_ms"] > 0
         assert abs(st["conv"]["flops"] / 32 - info["flops_per_image"]) / info["flops_per_image"] < 0.01
+
+
+def test_graph_replays_match_the_eager_pass():
+    # The pass is recorded once per batch size and buffer set and replayed
+    # from then on; every replay, with eager work and synchronisations in
+    # between, gives the bits of the eager pass, and each batch size keeps
+    # its own recording.
+    import torch
+    w = wl.workload("resnet18x3_bf16_b32")
+    imgs = _images(w)[:12]
+    with _ensemble(w, max_batch=32) as ens:
+        fsb.fs_graphs_enable(ens.handle, False)
+        ref = ens.infer(imgs)
+        ref5 = ens.infer(imgs[:5], want_mean=False)
+        fsb.fs_graphs_enable(ens.handle, True)
+        x = np.random.default_rng(3).standard_normal((2, 9, 9, 16)).astype(np.float32)
+        pool_ref = fsb.fs_test_maxpool(x, 3, 2, 1, fsb.FS_F32)
+        for i in range(4):
+            g = ens.infer(imgs)
+            for k in ("probs", "logits", "vote", "top1", "mean"):
+                assert np.array_equal(g[k], ref[k]), (i, k)
+            g5 = ens.infer(imgs[:5], want_mean=False)
+            for k in ("probs", "logits", "vote", "top1"):
+                assert np.array_equal(g5[k], ref5[k]), (i, k)
+            assert np.array_equal(fsb.fs_test_maxpool(x, 3, 2, 1, fsb.FS_F32), pool_ref)
+            torch.cuda.synchronize()
