@@ -214,7 +214,7 @@ __device__ __forceinline__ TileCoord tile_coord(const ConvArgs& a, int bid) {
 template <int BM, int BN, int WGM, int WGN, int STAGES>
 __global__ void __launch_bounds__(64 * WGM * WGN,
                                   (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
-  constexpr int NW = WGM * WGN, NTH = 64 * NW;
+  constexpr int NW = WGM * WGN;
   constexpr int TM = BM / WGM, TN = BN / WGN;
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int AP = BM / (8 * NW), BP = BN / (8 * NW);  // DMA instructions per wave per tile
@@ -473,8 +473,7 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
   issue_patch(t_begin, 0, 0);
   // every step ends with NSTORE stores (dropped ones where no tile ends), so
   // every step starts with the same count of stores in flight behind its patch
-#pragma unroll
-  for (int u = 0; u < NSTORE; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
+  dummy_stores<NSTORE>(ry);
   for (int st = 0; st < steps; ++st) {
     const int tj = st / CH, cc = st - tj * CH;
     wait_vmcnt<NSTORE>();  // the patch landed; the last step's stores may be in flight
@@ -516,8 +515,7 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
       mma_ktile_rows_sw<FM, FN>(Pb, wsm, ra, sa, rb, lane, acc);
     }
     if (cc != CH - 1) {
-#pragma unroll
-      for (int u = 0; u < NSTORE; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
+      dummy_stores<NSTORE>(ry);
     } else {  // epilogue: bias, residual, ReLU, bf16, 16-byte stores
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -545,7 +543,8 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
 #pragma unroll
               for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
             const int n = n0 + j * 32 + 8 * (gp + fq);
-            const uint32_t off = mg[i] >= 0 ? (uint32_t)(((int64_t)mg[i] * a.Cout + n) * 2) : OOB;
+            const uint32_t off = mg[i] >= 0 ? (uint32_t)(((int64_t)mg[i] * a.Cout + n) * 2)
+                                            : OOB + 16u * (uint32_t)((i * FN + j) * 2 + h);  // distinct: never merged
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry, off, 0, 0);
           }
       zero_acc();
@@ -802,8 +801,7 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
   issue_patch(step_img(0), step_rho(0), psm0);
   // STEM_NSTORE dropped stores, so that every step starts with the same count
   // of stores in flight behind its rows
-#pragma unroll
-  for (int u = 0; u < STEM_NSTORE; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
+  dummy_stores<STEM_NSTORE>(ry);
   for (int st = 0; st < nsteps; st += 2) {
     do_step(st, psm0, psm1);
     if (st + 1 < nsteps) do_step(st + 1, psm1, psm0);

@@ -325,8 +325,7 @@ __global__ void __launch_bounds__(64 * HS_NW, 1) k_conv_hs(ConvArgs a) {
   read_frags(wa0, ps0, q0c, h0c, 0, 0, Fa, 1);
   issue_slice(std::integral_constant<int, 0>{}, ps1, poA, 1);
   issue_w(ws2, 2 * CH + 0);
-#pragma unroll
-  for (int u = 0; u < HS_SI; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, ry, OOB, 0, 0);
+  dummy_stores<HS_SI>(ry);
 
   uint4 res_v[2][2][2];
   int ge = 0;  // even chunk of the current pair, counted over the workgroup's tiles
@@ -452,7 +451,8 @@ __global__ void __launch_bounds__(64 * HS_NW, 1) k_conv_hs(ConvArgs a) {
 #pragma unroll
                   for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
                 const int n = n0 + wn * 64 + j * 32 + 8 * (gp + fq);
-                const uint32_t off = (last && mgc[i] >= 0) ? (uint32_t)(((int64_t)mgc[i] * a.Cout + n) * 2) : OOB;
+                const uint32_t off = (last && mgc[i] >= 0) ? (uint32_t)(((int64_t)mgc[i] * a.Cout + n) * 2)
+                                                           : OOB + 16u * (uint32_t)((i * 2 + j) * 2 + h);  // distinct: never merged
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry, off, 0, 0);
               }
         }

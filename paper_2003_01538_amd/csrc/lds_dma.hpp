@@ -35,6 +35,16 @@ __device__ __forceinline__ void wait_vmcnt() {
 // s_waitcnt lgkmcnt(0), leaving vmcnt and expcnt alone
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4)); }
 
+// N stores that write nothing (buffer offsets past every range), for steps
+// that wait on a fixed vector-memory count.  Each goes to a different offset:
+// identical stores to one address would be merged by the compiler, leaving
+// fewer in flight than the count assumes and releasing the wait early.
+template <int N>
+__device__ __forceinline__ void dummy_stores(__amdgpu_buffer_rsrc_t r) {
+#pragma unroll
+  for (int u = 0; u < N; ++u) __builtin_amdgcn_raw_buffer_store_b128(v4u{0, 0, 0, 0}, r, OOB + 16u * u, 0, 0);
+}
+
 // Workgroup barrier without a memory fence (so it does not wait for vector
 // memory operations); the compiler may not move memory accesses across it.
 __device__ __forceinline__ void wg_barrier() {

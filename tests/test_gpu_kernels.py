@@ -181,6 +181,33 @@ def test_conv_repeat_is_bit_identical(gpu_lib):
         assert np.array_equal(fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16), g0)
 
 
+@pytest.mark.parametrize("kind", ["halo", "hs", "stem"])
+def test_persistent_kernels_repeat_bit_identical(gpu_lib, kind):
+    # The persistent kernels wait on fixed vector-memory counts; if the
+    # compiler drops or merges any of the loads and stores those counts
+    # assume, a step can start before its operands have landed and results
+    # vary from run to run.  Identical inputs must give identical bits, at a
+    # batch where each workgroup walks only two or three tiles (first steps
+    # weigh most).
+    rng = np.random.default_rng(11)
+    if kind == "stem":
+        x = oracle.round_bf16(rng.standard_normal((16, 224, 224, 3)).astype(np.float32))
+        w = oracle.round_bf16((rng.standard_normal((64, 7, 7, 3)) * np.sqrt(2.0 / 147)).astype(np.float32))
+        b = (rng.standard_normal(64) * 0.1).astype(np.float32)
+        run = lambda: fsb.fs_test_stem_pool(x, w, b)
+    else:
+        B, H, Ci, Co = (16, 56, 64, 64) if kind == "halo" else (16, 7, 512, 512)
+        x = oracle.round_bf16(rng.standard_normal((B, H, H, Ci)).astype(np.float32))
+        w = oracle.round_bf16((rng.standard_normal((Co, 3, 3, Ci)) * np.sqrt(2.0 / (9 * Ci))).astype(np.float32))
+        b = (rng.standard_normal(Co) * 0.1).astype(np.float32)
+        r = oracle.round_bf16(rng.standard_normal((B, H, H, Co)).astype(np.float32))
+        t = _tile_index("halo_4x56" if kind == "halo" else "hs_128x128")
+        run = lambda: fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16, tile=t)
+    g0 = run()
+    for i in range(12):
+        assert np.array_equal(run().view(np.uint32), g0.view(np.uint32)), i
+
+
 @pytest.mark.parametrize("B,H,W", [(2, 32, 32), (1, 224, 224), (3, 30, 20), (1, 2, 6)])
 def test_stem_conv_maxpool_fused(gpu_lib, B, H, W):
     # the fused stem equals the conv and the max pool run separately, bit for
