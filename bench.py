@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (scales the HBM byte "
                          "counters of a profiler run) and exit")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="launch every kernel of a step from the host instead of replaying the recorded pass")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
@@ -120,6 +122,8 @@ def main():
     imgs = list(wl.images_uniform(w["image_seed"], B, *w["in_hw"]))
     ens = fsb.Ensemble(w["models"], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"],
                        max_batch=B)
+    if args.no_graphs:
+        fsb.fs_graphs_enable(ens.handle, False)
     info = ens.info()
     N, C = info["num_models"], info["num_classes"]
 
