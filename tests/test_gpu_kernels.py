@@ -100,9 +100,10 @@ CONV_CASES = [
     (3, 2, 23, 128, 128, 3, 1, 1, 1, 0),   # streamed-weight halo, 40-block patch, tiles across images
     (1, 4, 70, 128, 128, 3, 1, 1, 1, 1),   # streamed-weight halo with its largest patch (48 blocks)
     (2, 5, 70, 128, 128, 3, 1, 1, 1, 0),   # patch too large for it: the implicit GEMM takes the layer
+    (4, 64, 64, 128, 256, 3, 1, 1, 1, 1),  # streamed-weight halo, 256 tiles of 128 x 128
 ]
 # cases the streamed-weight halo kernel (3x3/1, Cin and Cout multiples of 128) fits
-HS_CASES = (5, 10, 11, 12, 13, 14)
+HS_CASES = (5, 10, 11, 12, 13, 14, 16)
 
 
 def _conv_inputs(case, prec, seed):
@@ -181,14 +182,14 @@ def test_conv_repeat_is_bit_identical(gpu_lib):
         assert np.array_equal(fsb.fs_test_conv(x, w, b, r, 1, 1, 1, BF16), g0)
 
 
-@pytest.mark.parametrize("kind", ["halo", "hs", "stem"])
+@pytest.mark.parametrize("kind", ["halo", "hs", "hs_large", "stem"])
 def test_persistent_kernels_repeat_bit_identical(gpu_lib, kind):
     # The persistent kernels wait on fixed vector-memory counts; if the
     # compiler drops or merges any of the loads and stores those counts
     # assume, a step can start before its operands have landed and results
     # vary from run to run.  Identical inputs must give identical bits, at a
     # batch where each workgroup walks only two or three tiles (first steps
-    # weigh most).
+    # weigh most); "hs_large" has 256 tiles of 128 x 128.
     rng = np.random.default_rng(11)
     if kind == "stem":
         x = oracle.round_bf16(rng.standard_normal((16, 224, 224, 3)).astype(np.float32))
@@ -196,7 +197,7 @@ def test_persistent_kernels_repeat_bit_identical(gpu_lib, kind):
         b = (rng.standard_normal(64) * 0.1).astype(np.float32)
         run = lambda: fsb.fs_test_stem_pool(x, w, b)
     else:
-        B, H, Ci, Co = (16, 56, 64, 64) if kind == "halo" else (16, 7, 512, 512)
+        B, H, Ci, Co = {"halo": (16, 56, 64, 64), "hs": (16, 7, 512, 512), "hs_large": (4, 64, 128, 256)}[kind]
         x = oracle.round_bf16(rng.standard_normal((B, H, H, Ci)).astype(np.float32))
         w = oracle.round_bf16((rng.standard_normal((Co, 3, 3, Ci)) * np.sqrt(2.0 / (9 * Ci))).astype(np.float32))
         b = (rng.standard_normal(Co) * 0.1).astype(np.float32)
