@@ -43,6 +43,8 @@ def parse():
                          "counters of a profiler run) and exit")
     ap.add_argument("--no-graphs", action="store_true",
                     help="launch every kernel of a step from the host instead of replaying the recorded pass")
+    ap.add_argument("--combine", default="mean", choices=["mean", "plurality", "any"],
+                    help="combine policy of vote (any: class 0 detected by at least one model)")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
@@ -124,6 +126,9 @@ def main():
                        max_batch=B)
     if args.no_graphs:
         fsb.fs_graphs_enable(ens.handle, False)
+    if args.combine != "mean":
+        policy = {"plurality": fsb.FS_COMBINE_PLURALITY, "any": fsb.FS_COMBINE_ANY}[args.combine]
+        fsb.fs_set_combine(ens.handle, policy, 0, 1)
     info = ens.info()
     N, C = info["num_models"], info["num_classes"]
 
@@ -198,6 +203,7 @@ def main():
         "data": "synthetic: seeded uint8 noise images, He-normal random weights",
         "config": {"workload": w["name"], "models": list(w["archs"]), "batch": B,
                    "input_hw": list(w["in_hw"]), "transformed_hw": list(w["out_hw"]),
+                   "combine": args.combine,
                    "flops_per_image": info["flops_per_image"],
                    "launches_per_step": info["launches_per_pass"]},
         "roofline": roof,

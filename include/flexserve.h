@@ -44,7 +44,19 @@ typedef enum {
 
 typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_precision; /* storage type of the whole ensemble */
 typedef enum { FS_OP_CONV = 0, FS_OP_MAXPOOL = 1, FS_OP_GAP = 2, FS_OP_FC = 3 } fs_op;
-typedef enum { FS_COMBINE_MEAN = 0 } fs_combine;     /* mean of the models' probabilities */
+/* How vote[b] combines the models' outputs for image b (Sec. 2.1: outputs
+ * are combined according to the consumer's policy).
+ *   FS_COMBINE_MEAN       the smallest class maximising sum_i probs[i][b][c]
+ *                         (the argmax of the mean probability)
+ *   FS_COMBINE_PLURALITY  the class that is top-1 of the most models; among
+ *                         classes with equally many, the smallest
+ *   FS_COMBINE_ANY        sensitivity policy for one designated class c*:
+ *                         model i detects c* when its top-1 class is c*;
+ *                         vote[b] = 1 when at least k models detect it,
+ *                         else 0.  k = 1 is the maximum-sensitivity OR of
+ *                         the models' binary outputs (Sec. 2.1); k = N the
+ *                         AND.  Set with fs_set_combine. */
+typedef enum { FS_COMBINE_MEAN = 0, FS_COMBINE_PLURALITY = 1, FS_COMBINE_ANY = 2 } fs_combine;
 
 /* One layer, listed in topological order.  Layer outputs are referred to by
  * index; src = -1 is the shared transformed input batch (3 channels). */
@@ -83,7 +95,7 @@ typedef struct {
     const fs_model_spec *models;
     fs_preprocess pre;
     int32_t precision;  /* fs_precision */
-    int32_t combine;    /* fs_combine   */
+    int32_t combine;    /* fs_combine: MEAN or PLURALITY (ANY needs fs_set_combine) */
     int32_t max_batch;  /* largest batch one device pass handles (1..4096) */
     int32_t device;     /* HIP device ordinal */
 } fs_ensemble_desc;
@@ -116,7 +128,9 @@ fs_status fs_ensemble_create(const fs_ensemble_desc *desc, fs_ensemble **out);
  * synchronous.  B == 0 is a no-op.  B > max_batch is processed in chunks.
  *   probs      [N][B][C] fp32, required
  *   mean_probs [B][C]    fp32, optional (NULL)
- *   vote       [B]       int32, required: smallest c maximising sum_i probs[i][b][c]
+ *   vote       [B]       int32, required: the combined result of the current
+ *                         policy (fs_combine; by default the smallest c
+ *                         maximising sum_i probs[i][b][c])
  *   top1       [N][B]    int32, optional: smallest c maximising model i's logits
  *   logits     [N][B][C] fp32, optional */
 fs_status fs_infer(fs_ensemble *e, const fs_image *imgs, int32_t B,
@@ -141,6 +155,15 @@ fs_status fs_infer_device(fs_ensemble *e, const uint8_t *d_pixels,
  * stream.  enable = 0 turns graphs off and drops the recorded passes.
  * Synchronises the ensemble's stream.  FS_ERR_INVALID for a NULL handle. */
 fs_status fs_graphs_enable(fs_ensemble *e, int32_t enable);
+
+/* Combine policy of the following fs_infer / fs_infer_device calls
+ * (fs_combine).  positive_class (0 <= c* < num_classes) and min_votes
+ * (1 <= k <= num_models) are read for FS_COMBINE_ANY only.  probs, mean and
+ * top1 do not depend on the policy.  Synchronises the ensemble's stream and
+ * drops its recorded graphs.  FS_ERR_INVALID for a NULL handle, an unknown
+ * policy or parameters out of range; FS_ERR_UNSUPPORTED for PLURALITY with
+ * more than 64 models. */
+fs_status fs_set_combine(fs_ensemble *e, int32_t policy, int32_t positive_class, int32_t min_votes);
 
 void fs_destroy(fs_ensemble *e); /* NULL-safe; waits for outstanding work */
 
@@ -238,6 +261,11 @@ fs_status fs_test_fc(const float *in, int32_t B, int32_t K, const float *w, cons
 fs_status fs_test_softmax_combine(const float *logits, int32_t N, int32_t B, int32_t C,
                                   float *probs, float *mean, int32_t *vote, int32_t *top1,
                                   int32_t device);
+/* The same with a combine policy and its parameters (see fs_set_combine). */
+fs_status fs_test_softmax_combine_policy(const float *logits, int32_t N, int32_t B, int32_t C,
+                                         int32_t policy, int32_t positive_class, int32_t min_votes,
+                                         float *probs, float *mean, int32_t *vote, int32_t *top1,
+                                         int32_t device);
 
 /* Measurement of one convolution layer shape: Z models' weights, one
  * shared input filled with a constant, `iters` back-to-back launches of tile

@@ -68,6 +68,7 @@ def lib():
         L.fso_softmax.argtypes = [P, I, I, P]
         L.fso_argmax.argtypes = [P, I]
         L.fso_combine.argtypes = [P, P, I, I, I, P, P, P, P]
+        L.fso_vote_policy.argtypes = [P, I, I, I, I, I, I, P]
         _lib = L
     return _lib
 
@@ -188,6 +189,19 @@ def combine(p, z=None):
     lib().fso_combine(_p(p), _p(zc), N, B, C, _p(S), _p(mean), _p(vote),
                       _p(top1) if zc is not None else None)
     return dict(S=S, mean=mean, vote=vote, top1=top1 if zc is not None else None)
+
+
+PLURALITY, ANY = 1, 2
+
+
+def vote_policy(top1, C, policy, pos=0, k=1):
+    """top1 [N, B] -> [B]: plurality (policy 1) or detection of class `pos`
+    by at least k models (policy 2; k = 1 is the OR of Sec. 2.1)."""
+    t = np.ascontiguousarray(top1, np.int32)
+    N, B = t.shape
+    out = np.empty(B, np.int32)
+    lib().fso_vote_policy(_p(t), N, B, int(C), int(policy), int(pos), int(k), _p(out))
+    return out
 
 
 # ------------------------------------------------------------- networks

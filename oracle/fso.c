@@ -19,7 +19,9 @@
  *   avg pool   mean over all H*W positions
  *   fc         z = b + W f
  *   softmax    p_j = exp(z_j - max z) / sum_k exp(z_k - max z)
- *   combine    S = sum over models of p, mean = S/N, vote = argmax S
+ *   combine    S = sum over models of p, mean = S/N, vote = argmax S;
+ *              or, from the models' top-1 classes, plurality or detection
+ *              of one class by at least k models (fso_vote_policy)
  *
  * Arithmetic: every sum is accumulated in double precision, and each value
  * the GPU path *stores* is rounded to the storage type at that point:
@@ -309,5 +311,32 @@ void fso_combine(const float *p, const float *z, int N, int B, int C,
         if (z && top1)
             for (int i = 0; i < N; ++i)
                 top1[(int64_t)i * B + b] = fso_argmax(z + ((int64_t)i * B + b) * C, C);
+    }
+}
+
+/* Combined result from the models' top-1 classes top1 [N][B] (Sec. 2.1: the
+ * consumer combines the outputs by its own policy).
+ *   policy 1, plurality: out[b] = the class named top-1 by the most models,
+ *     the smallest such class when several are named equally often; found
+ *     by counting the votes of every class 0..C-1.
+ *   policy 2, detection of class pos: model i reports y_i = 1 when its top-1
+ *     class is pos; out[b] = 1 when at least k of the y_i are 1.  k = 1 is
+ *     y_1 | y_2 | ... | y_N, the maximum-sensitivity policy. */
+void fso_vote_policy(const int32_t *top1, int N, int B, int C, int policy, int pos, int k, int32_t *out)
+{
+    for (int b = 0; b < B; ++b) {
+        if (policy == 2) {
+            int yes = 0;
+            for (int i = 0; i < N; ++i) yes += top1[(int64_t)i * B + b] == pos;
+            out[b] = yes >= k;
+        } else {
+            int best = 0, best_votes = -1;
+            for (int c = 0; c < C; ++c) {
+                int votes = 0;
+                for (int i = 0; i < N; ++i) votes += top1[(int64_t)i * B + b] == c;
+                if (votes > best_votes) { best_votes = votes; best = c; }
+            }
+            out[b] = best;
+        }
     }
 }

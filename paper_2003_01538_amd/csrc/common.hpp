@@ -122,8 +122,12 @@ struct SoftmaxArgs {
   int32_t* vote;        // [B]
   int32_t* top1;        // [N][B] or null
   int N, B, C;
+  int policy = 0;       // fs_combine of vote
+  int pos_class = 0;    // FS_COMBINE_ANY: the designated class
+  int min_votes = 1;    // FS_COMBINE_ANY: models that must detect it
 };
 constexpr int SOFTMAX_MAX_C = 4096;
+constexpr int COMBINE_MAX_PLURALITY = 64;  // most models FS_COMBINE_PLURALITY takes
 void launch_softmax_combine(const SoftmaxArgs& a, hipStream_t s);
 
 }  // namespace fs

@@ -151,6 +151,7 @@ struct fs_ensemble {
   int device = 0, num_cus = 256;
   Prec prec = BF16;
   int N = 0, C = 0, max_batch = 0;
+  int combine = FS_COMBINE_MEAN, pos_class = 0, min_votes = 1;  // policy of vote
   fs_preprocess pre{};
   std::vector<Group> groups;
   double flops_per_image = 0;
@@ -185,11 +186,27 @@ namespace {
 size_t es(Prec p) { return p == BF16 ? 2 : 4; }
 
 // ----------------------------------------------------------- validation
+// Checks a combine policy and its parameters for N models of C classes.
+void check_combine(int policy, int pos_class, int min_votes, int N, int C) {
+  if (policy != FS_COMBINE_MEAN && policy != FS_COMBINE_PLURALITY && policy != FS_COMBINE_ANY)
+    fail(FS_ERR_INVALID, "unknown combine policy " + std::to_string(policy));
+  if (policy == FS_COMBINE_PLURALITY && N > COMBINE_MAX_PLURALITY)
+    fail(FS_ERR_UNSUPPORTED, "FS_COMBINE_PLURALITY takes at most 64 models");
+  if (policy == FS_COMBINE_ANY && (pos_class < 0 || pos_class >= C))
+    fail(FS_ERR_INVALID, "positive_class must be in 0..num_classes-1");
+  if (policy == FS_COMBINE_ANY && (min_votes < 1 || min_votes > N))
+    fail(FS_ERR_INVALID, "min_votes must be in 1..num_models");
+}
+
 void validate_desc(const fs_ensemble_desc* d) {
   if (!d) fail(FS_ERR_INVALID, "desc is NULL");
   if (d->num_models < 1 || !d->models) fail(FS_ERR_INVALID, "num_models must be >= 1 with a models array");
   if (d->precision != FS_F32 && d->precision != FS_BF16) fail(FS_ERR_INVALID, "precision must be FS_F32 or FS_BF16");
-  if (d->combine != FS_COMBINE_MEAN) fail(FS_ERR_UNSUPPORTED, "only FS_COMBINE_MEAN is supported");
+  if (d->combine != FS_COMBINE_MEAN && d->combine != FS_COMBINE_PLURALITY)
+    fail(FS_ERR_INVALID, "combine must be FS_COMBINE_MEAN or FS_COMBINE_PLURALITY at create "
+                         "(FS_COMBINE_ANY takes its class and count through fs_set_combine)");
+  if (d->combine == FS_COMBINE_PLURALITY && d->num_models > COMBINE_MAX_PLURALITY)
+    fail(FS_ERR_UNSUPPORTED, "FS_COMBINE_PLURALITY takes at most 64 models");
   if (d->max_batch < 1 || d->max_batch > 4096) fail(FS_ERR_INVALID, "max_batch must be in 1..4096");
   if (d->pre.out_h < 1 || d->pre.out_w < 1 || d->pre.out_h > 4096 || d->pre.out_w > 4096)
     fail(FS_ERR_INVALID, "preprocess output size must be in 1..4096");
@@ -500,6 +517,7 @@ void set_device(int dev) {
 void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   e->prec = d->precision == FS_BF16 ? BF16 : F32;
   e->N = d->num_models;
+  e->combine = d->combine;
   e->C = d->models[0].num_classes;
   e->max_batch = d->max_batch;
   e->pre = d->pre;
@@ -842,6 +860,9 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
   sa.N = e->N;
   sa.B = B;
   sa.C = e->C;
+  sa.policy = e->combine;
+  sa.pos_class = e->pos_class;
+  sa.min_votes = e->min_votes;
   const double sbytes = (double)e->N * B * e->C * 8 + (d_mean ? (double)B * e->C * 4 : 0) + B * 4.0;
   launch(K_SOFTMAX, 0.0, sbytes, 1, [&] { launch_softmax_combine(sa, s); });
   HIPCHK(hipGetLastError());
@@ -1174,6 +1195,23 @@ fs_status fs_graphs_enable(fs_ensemble* e, int32_t enable) {
   });
 }
 
+fs_status fs_set_combine(fs_ensemble* e, int32_t policy, int32_t positive_class, int32_t min_votes) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    check_combine(policy, positive_class, min_votes, e->N, e->C);
+    HIPCHK(hipSetDevice(e->device));
+    HIPCHK(hipStreamSynchronize(e->stream));
+    clear_graphs(e);  // the recorded passes carry the old policy's arguments
+    e->combine = policy;
+    e->pos_class = policy == FS_COMBINE_ANY ? positive_class : 0;
+    e->min_votes = policy == FS_COMBINE_ANY ? min_votes : 1;
+  });
+}
+
 fs_status fs_profile_enable(fs_ensemble* e, int32_t enable) {
   if (!e) {
     g_thread_error = "ensemble is NULL";
@@ -1460,9 +1498,16 @@ fs_status fs_test_fc(const float* in, int32_t B, int32_t K, const float* w, cons
 
 fs_status fs_test_softmax_combine(const float* logits, int32_t N, int32_t B, int32_t C, float* probs, float* mean,
                                   int32_t* vote, int32_t* top1, int32_t device) {
+  return fs_test_softmax_combine_policy(logits, N, B, C, FS_COMBINE_MEAN, 0, 1, probs, mean, vote, top1, device);
+}
+
+fs_status fs_test_softmax_combine_policy(const float* logits, int32_t N, int32_t B, int32_t C, int32_t policy,
+                                         int32_t positive_class, int32_t min_votes, float* probs, float* mean,
+                                         int32_t* vote, int32_t* top1, int32_t device) {
   return guarded(nullptr, [&] {
     if (!logits || !probs || !vote || N < 1 || B < 1 || C < 1) fail(FS_ERR_INVALID, "bad softmax arguments");
     if (C > SOFTMAX_MAX_C) fail(FS_ERR_UNSUPPORTED, "more than 4096 classes");
+    check_combine(policy, positive_class, min_votes, N, C);
     set_device(device);
     TmpDev t;
     const size_t n = (size_t)N * B * C;
@@ -1479,6 +1524,7 @@ fs_status fs_test_softmax_combine(const float* logits, int32_t N, int32_t B, int
     a.vote = static_cast<int32_t*>(dv);
     a.top1 = top1 ? static_cast<int32_t*>(dt) : nullptr;
     a.N = N; a.B = B; a.C = C;
+    a.policy = policy; a.pos_class = positive_class; a.min_votes = min_votes;
     launch_softmax_combine(a, nullptr);
     HIPCHK(hipGetLastError());
     HIPCHK(hipDeviceSynchronize());

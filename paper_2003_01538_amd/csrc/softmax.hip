@@ -8,11 +8,33 @@
 // probabilities are written and added into per-thread running sums S[c]
 // (fp32, model order).  After the last model the same reduction picks the
 // vote = smallest c maximising S, and mean = S / N is written.  One launch,
-// logits read once, probabilities written once.
+// logits read once, probabilities written once.  The other combine
+// policies decide vote from the models' top-1 classes, gathered in LDS:
+// plurality (the class most models rank first, the smallest among equally
+// many) or detection of one class by at least k models (k = 1: the
+// maximum-sensitivity OR of Sec. 2.1).
 #include "common.hpp"
 #include "device.hpp"
 
+#include "flexserve.h"
+
 namespace fs {
+
+// vote of a top-1 policy from the N models' top-1 classes (one thread)
+__device__ int policy_vote(const SoftmaxArgs& a, const int* tops) {
+  if (a.policy == FS_COMBINE_ANY) {
+    int n = 0;
+    for (int m = 0; m < a.N; ++m) n += tops[m] == a.pos_class ? 1 : 0;
+    return n >= a.min_votes ? 1 : 0;
+  }
+  int best = a.C, best_n = 0;  // FS_COMBINE_PLURALITY
+  for (int m = 0; m < a.N; ++m) {
+    int n = 0;
+    for (int k = 0; k < a.N; ++k) n += tops[k] == tops[m] ? 1 : 0;
+    if (n > best_n || (n == best_n && tops[m] < best)) { best_n = n; best = tops[m]; }
+  }
+  return best;
+}
 
 constexpr int SM_T = 256;
 constexpr int SM_PER = SOFTMAX_MAX_C / SM_T;  // classes per thread, upper bound
@@ -45,6 +67,8 @@ template <int PER>
 __global__ void __launch_bounds__(SM_T) k_softmax_combine(SoftmaxArgs a) {
   __shared__ float sv[SM_T / 64];
   __shared__ int si[SM_T / 64];
+  __shared__ int tops[COMBINE_MAX_PLURALITY];
+  int n_pos = 0;  // models whose top-1 is the designated class (thread 0)
   const int b = blockIdx.x, tid = threadIdx.x;
   float S[PER], z[PER];
 #pragma unroll
@@ -62,6 +86,10 @@ __global__ void __launch_bounds__(SM_T) k_softmax_combine(SoftmaxArgs a) {
     }
     block_argmax(best, bi, sv, si);
     if (a.top1 && tid == 0) a.top1[(int64_t)m * a.B + b] = bi;
+    if (tid == 0) {
+      if (m < COMBINE_MAX_PLURALITY) tops[m] = bi;
+      n_pos += bi == a.pos_class ? 1 : 0;
+    }
     float e[PER], part = 0.f;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -89,7 +117,11 @@ __global__ void __launch_bounds__(SM_T) k_softmax_combine(SoftmaxArgs a) {
     if (c < a.C && (S[j] > best || (S[j] == best && c < bi))) { best = S[j]; bi = c; }
   }
   block_argmax(best, bi, sv, si);
-  if (tid == 0) a.vote[b] = bi;
+  if (tid == 0) {
+    if (a.policy == FS_COMBINE_ANY) a.vote[b] = n_pos >= a.min_votes ? 1 : 0;
+    else if (a.policy == FS_COMBINE_PLURALITY) a.vote[b] = policy_vote(a, tops);
+    else a.vote[b] = bi;
+  }
   if (a.mean) {
     const float invn = (float)a.N;
 #pragma unroll
@@ -111,6 +143,7 @@ __global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a)
   __shared__ float ps[NG][PER * SM_T];
   __shared__ float sv[NG * W];
   __shared__ int si[NG * W];
+  __shared__ int tops[NG];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int g = tid / SM_T, t = tid - g * SM_T, lane = tid & 63, wave = tid >> 6;
   const bool live = g < a.N;
@@ -131,6 +164,7 @@ __global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a)
   for (int w = 1; w < W; ++w)
     if (sv[g * W + w] > best || (sv[g * W + w] == best && si[g * W + w] < bi)) { best = sv[g * W + w]; bi = si[g * W + w]; }
   if (live && a.top1 && t == 0) a.top1[(int64_t)g * a.B + b] = bi;
+  if (live && t == 0) tops[g] = bi;  // read after the barriers below
   float e[PER], part = 0.f;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
@@ -174,7 +208,7 @@ __global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a)
     int i = si[0];
     for (int w = 1; w < NG * W; ++w)
       if (sv[w] > v || (sv[w] == v && si[w] < i)) { v = sv[w]; i = si[w]; }
-    a.vote[b] = i;
+    a.vote[b] = a.policy == FS_COMBINE_MEAN ? i : policy_vote(a, tops);
   }
 }
 

@@ -23,7 +23,7 @@ LIB_PATH = os.path.join(HERE, "libflexserve.so")
 FS_OK, FS_ERR_INVALID, FS_ERR_OOM, FS_ERR_DEVICE, FS_ERR_UNSUPPORTED, FS_ERR_INTERNAL = range(6)
 FS_F32, FS_BF16 = 0, 1
 FS_OP_CONV, FS_OP_MAXPOOL, FS_OP_GAP, FS_OP_FC = range(4)
-FS_COMBINE_MEAN = 0
+FS_COMBINE_MEAN, FS_COMBINE_PLURALITY, FS_COMBINE_ANY = range(3)
 STATUS_NAMES = {0: "FS_OK", 1: "FS_ERR_INVALID", 2: "FS_ERR_OOM", 3: "FS_ERR_DEVICE",
                 4: "FS_ERR_UNSUPPORTED", 5: "FS_ERR_INTERNAL"}
 
@@ -98,6 +98,7 @@ SIGNATURES = [
     ("fs_query", ctypes.c_int, [_vp, ctypes.POINTER(fs_info)]),
     ("fs_profile_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
     ("fs_graphs_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
+    ("fs_set_combine", ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
     ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
@@ -115,6 +116,8 @@ SIGNATURES = [
                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _fp, ctypes.c_int32]),
     ("fs_test_softmax_combine", ctypes.c_int, [_fp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                _fp, _fp, _i32p, _i32p, ctypes.c_int32]),
+    ("fs_test_softmax_combine_policy", ctypes.c_int, [_fp] + [ctypes.c_int32] * 6 +
+                                                     [_fp, _fp, _i32p, _i32p, ctypes.c_int32]),
     ("fs_bench_conv", ctypes.c_int, [ctypes.c_int32] * 15 + [ctypes.POINTER(ctypes.c_double), _i32p,
                                                          ctypes.c_int32]),
     ("fs_conv_num_tiles", ctypes.c_int32, [ctypes.c_int32]),
@@ -168,7 +171,7 @@ def _check(st, handle=None):
 _OPS = {"conv": FS_OP_CONV, "maxpool": FS_OP_MAXPOOL, "gap": FS_OP_GAP, "fc": FS_OP_FC}
 
 
-def make_desc(models, out_hw, mean, std, precision, max_batch, device=0):
+def make_desc(models, out_hw, mean, std, precision, max_batch, device=0, combine=FS_COMBINE_MEAN):
     """Marshal layer dictionaries (see the ``workloads`` module) into an
     fs_ensemble_desc.  Returns (desc, keepalive)."""
     keep = []
@@ -208,7 +211,7 @@ def make_desc(models, out_hw, mean, std, precision, max_batch, device=0):
         d.pre.mean[c] = mean[c]
         d.pre.std[c] = std[c]
     d.precision = {"fp32": FS_F32, "bf16": FS_BF16}.get(precision, precision)
-    d.combine = FS_COMBINE_MEAN
+    d.combine = combine
     d.max_batch = max_batch
     d.device = device
     keep.append(specs)
@@ -273,6 +276,10 @@ def fs_query(handle) -> dict:
 
 def fs_graphs_enable(handle, enable=True):
     _check(load().fs_graphs_enable(handle, int(bool(enable))), handle)
+
+
+def fs_set_combine(handle, policy, positive_class=0, min_votes=1):
+    _check(load().fs_set_combine(handle, int(policy), int(positive_class), int(min_votes)), handle)
 
 
 def fs_profile_enable(handle, enable=True):
@@ -376,6 +383,19 @@ def fs_test_softmax_combine(logits, device=0):
     return dict(probs=probs, mean=mean, vote=vote, top1=top1)
 
 
+def fs_test_softmax_combine_policy(logits, policy, positive_class=0, min_votes=1, device=0):
+    z = np.ascontiguousarray(logits, np.float32)
+    N, B, C = z.shape
+    probs = np.zeros_like(z)
+    mean = np.zeros((B, C), np.float32)
+    vote = np.zeros(B, np.int32)
+    top1 = np.zeros((N, B), np.int32)
+    _check(load().fs_test_softmax_combine_policy(_f(z), N, B, C, int(policy), int(positive_class),
+                                                 int(min_votes), _f(probs), _f(mean), _i(vote), _i(top1),
+                                                 device))
+    return dict(probs=probs, mean=mean, vote=vote, top1=top1)
+
+
 def fs_bench_conv(B, H, W, Cin, Cout, k, stride, pad, relu=1, residual=0, precision=FS_BF16, tile=-1,
                   Z=1, iters=20, device=0):
     """Mean time (ms) of one launch of the conv kernel on this shape, and the
@@ -400,8 +420,9 @@ def fs_conv_tile_name(precision, tile) -> str:
 class Ensemble:
     """An ensemble handle built from layer dictionaries."""
 
-    def __init__(self, models, out_hw, mean, std, precision="bf16", max_batch=256, device=0):
-        desc, keep = make_desc(models, out_hw, mean, std, precision, max_batch, device)
+    def __init__(self, models, out_hw, mean, std, precision="bf16", max_batch=256, device=0,
+                 combine=FS_COMBINE_MEAN):
+        desc, keep = make_desc(models, out_hw, mean, std, precision, max_batch, device, combine)
         self.handle = fs_ensemble_create(desc)
         self.N = len(models)
         self.C = models[0][-1]["cout"]
@@ -412,6 +433,9 @@ class Ensemble:
 
     def info(self):
         return fs_query(self.handle)
+
+    def set_combine(self, policy, positive_class=0, min_votes=1):
+        fs_set_combine(self.handle, policy, positive_class, min_votes)
 
     def close(self):
         if self.handle:

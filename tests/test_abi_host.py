@@ -57,11 +57,12 @@ def _create_status(desc):
     return st, h.value, fsb.fs_last_error(None)
 
 
-def test_create_valid_without_device_reports_device_error():
+@pytest.mark.parametrize("combine", [fsb.FS_COMBINE_MEAN, fsb.FS_COMBINE_PLURALITY])
+def test_create_valid_without_device_reports_device_error(combine):
     import torch
     if torch.cuda.is_available():
         pytest.skip("a device is present")
-    d, keep = _tiny_desc()
+    d, keep = _tiny_desc(combine=combine)
     st, h, msg = _create_status(d)
     assert st == fsb.FS_ERR_DEVICE and h is None and msg
 
@@ -80,6 +81,8 @@ def test_create_valid_without_device_reports_device_error():
     (dict(mutate={(0, 0): dict(cout=12), (0, 2): dict(cin=12)}), fsb.FS_ERR_UNSUPPORTED),
     (dict(mutate={(0, 4): dict(cin=31)}), fsb.FS_ERR_INVALID),           # fc fan-in
     (dict(mutate={(0, 1): dict(pad=2)}), fsb.FS_ERR_INVALID),            # pool pad >= k
+    (dict(combine=fsb.FS_COMBINE_ANY), fsb.FS_ERR_INVALID),              # its class comes from fs_set_combine
+    (dict(combine=9), fsb.FS_ERR_INVALID),
 ])
 def test_create_rejects_invalid_descriptors(case, status):
     d, keep = _tiny_desc(**case)
@@ -108,6 +111,7 @@ def test_calls_on_null_handle_fail_cleanly():
     assert lib.fs_query(None, None) == fsb.FS_ERR_INVALID
     assert lib.fs_profile_enable(None, 1) == fsb.FS_ERR_INVALID
     assert lib.fs_graphs_enable(None, 1) == fsb.FS_ERR_INVALID
+    assert lib.fs_set_combine(None, fsb.FS_COMBINE_PLURALITY, 0, 1) == fsb.FS_ERR_INVALID
     lib.fs_destroy(None)
 
 
@@ -123,6 +127,18 @@ def test_test_entries_validate_before_device():
     assert e.value.status == fsb.FS_ERR_INVALID
     with pytest.raises(fsb.FsError) as e:
         fsb.fs_test_softmax_combine(np.zeros((1, 1, 5000), np.float32))
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
+    z = np.zeros((3, 2, 10), np.float32)
+    for policy, pos, k, status in [(5, 0, 1, fsb.FS_ERR_INVALID),                     # unknown policy
+                                   (fsb.FS_COMBINE_ANY, 10, 1, fsb.FS_ERR_INVALID),   # class out of range
+                                   (fsb.FS_COMBINE_ANY, -1, 1, fsb.FS_ERR_INVALID),
+                                   (fsb.FS_COMBINE_ANY, 3, 0, fsb.FS_ERR_INVALID),    # k out of 1..N
+                                   (fsb.FS_COMBINE_ANY, 3, 4, fsb.FS_ERR_INVALID)]:
+        with pytest.raises(fsb.FsError) as e:
+            fsb.fs_test_softmax_combine_policy(z, policy, pos, k)
+        assert e.value.status == status, (policy, pos, k)
+    with pytest.raises(fsb.FsError) as e:
+        fsb.fs_test_softmax_combine_policy(np.zeros((65, 1, 10), np.float32), fsb.FS_COMBINE_PLURALITY)
     assert e.value.status == fsb.FS_ERR_UNSUPPORTED
     bad = [np.zeros((0, 4, 3), np.uint8)]
     with pytest.raises(fsb.FsError) as e:

@@ -192,3 +192,37 @@ def test_graph_replays_match_the_eager_pass():
                 assert np.array_equal(g5[k], ref5[k]), (i, k)
             assert np.array_equal(fsb.fs_test_maxpool(x, 3, 2, 1, fsb.FS_F32), pool_ref)
             torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("wname", ["tiny2_fp32_b4", "resnet18x3_bf16_b32"])
+def test_combine_policies_per_call(wname):
+    # The policy chosen with fs_set_combine decides vote from the models'
+    # top-1 classes exactly as the oracle's rule does; probabilities, mean
+    # and top-1 are untouched, a switch re-records the pass, and switching
+    # back restores the mean-probability vote.
+    w = wl.workload(wname)
+    imgs = _images(w)[:8] if w["batch"] >= 8 else _images(w)
+    with _ensemble(w) as ens:
+        ref = ens.infer(imgs)
+        N, C = ref["probs"].shape[0], ref["probs"].shape[2]
+        t = ref["top1"]
+        cases = [(fsb.FS_COMBINE_PLURALITY, 0, 1)]
+        for c in sorted({int(t[0, 0]), int(t[-1, -1]), C - 1}):
+            cases += [(fsb.FS_COMBINE_ANY, c, k) for k in sorted({1, N})]
+        for policy, pos, k in cases:
+            ens.set_combine(policy, pos, k)
+            for _ in range(2):  # recorded, then replayed
+                g = ens.infer(imgs)
+                for key in ("probs", "mean", "top1", "logits"):
+                    assert np.array_equal(g[key], ref[key]), (policy, key)
+                assert np.array_equal(g["vote"], oracle.vote_policy(t, C, policy, pos, k)), (policy, pos, k)
+        ens.set_combine(fsb.FS_COMBINE_MEAN)
+        assert np.array_equal(ens.infer(imgs)["vote"], ref["vote"])
+        with pytest.raises(fsb.FsError) as e:
+            ens.set_combine(fsb.FS_COMBINE_ANY, C, 1)
+        assert e.value.status == fsb.FS_ERR_INVALID
+    # plurality chosen when the ensemble is created
+    with fsb.Ensemble(w["models"], w["out_hw"], MEAN, STD, w["precision"], max_batch=w["batch"],
+                      combine=fsb.FS_COMBINE_PLURALITY) as ens:
+        g = ens.infer(imgs)
+        assert np.array_equal(g["vote"], oracle.vote_policy(g["top1"], C, fsb.FS_COMBINE_PLURALITY))

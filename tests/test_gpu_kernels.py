@@ -303,6 +303,28 @@ def test_softmax_combine_parity(gpu_lib, N, B, C, scale):
             assert S[b, g["vote"][b]] >= S[b].max() - 2 * N * 1e-6
 
 
+@pytest.mark.parametrize("N,C", [(1, 7), (3, 4), (4, 1000), (3, 2000), (6, 5), (9, 1000)])
+def test_combine_policies_match_the_oracle(gpu_lib, N, C):
+    # few classes make equal vote counts common; (3, 2000), (6, 5), (9, 1000)
+    # run the one-model-at-a-time kernel, the others the side-by-side one
+    B = 64
+    rng = np.random.default_rng(N * 7 + C)
+    z = rng.standard_normal((N, B, C)).astype(np.float32)
+    z[:, :4] = np.round(z[:, :4])  # exact logit ties: top-1 is the smallest maximising class
+    o = oracle.combine(oracle.softmax(z), z)
+    ref = fsb.fs_test_softmax_combine(z)
+    cases = [(fsb.FS_COMBINE_PLURALITY, 0, 1)] + [(fsb.FS_COMBINE_ANY, c, k) for c in (0, C // 2, C - 1)
+                                                  for k in sorted({1, (N + 1) // 2, N})]
+    for policy, pos, k in cases:
+        g = fsb.fs_test_softmax_combine_policy(z, policy, pos, k)
+        assert np.array_equal(g["top1"], o["top1"])
+        want = oracle.vote_policy(o["top1"], C, policy, pos, k)
+        assert np.array_equal(g["vote"], want), (policy, pos, k)
+        # probabilities, mean and top-1 do not depend on the policy
+        for key in ("probs", "mean", "top1"):
+            assert np.array_equal(g[key], ref[key]), key
+
+
 def test_softmax_combine_exact_ties_take_lowest_index(gpu_lib):
     z = np.full((2, 3, 50), -1e4, np.float32)
     z[0, :, 31] = 0.0   # model 0 saturates on 31

@@ -282,6 +282,55 @@ def test_combine_identical_models_and_ties():
     assert oracle.argmax(np.array([1, 5, 5, 2], np.float32)) == 1
 
 
+# Hand-worked combinations of top-1 lists (one column per image, one row per
+# model): plurality answers, and the detection policy of Sec. 2.1 for a class
+# c* and count k, worked out by reading each column.
+POLICY_TOP1 = np.array([[5, 7, 4, 1, 3],
+                        [5, 2, 4, 8, 3],
+                        [2, 9, 9, 8, 3],
+                        [6, 9, 9, 1, 3]], np.int32)
+POLICY_CASES = [  # (policy, c*, k, expected per column)
+    (oracle.PLURALITY, 0, 1, [5, 9, 4, 1, 3]),  # 2-1-1 / 2 nines / 4 vs 9 tie -> 4 / 1 vs 8 tie -> 1 / all 3
+    (oracle.ANY, 9, 1, [0, 1, 1, 0, 0]),        # OR: one model naming 9 is enough
+    (oracle.ANY, 9, 2, [0, 1, 1, 0, 0]),
+    (oracle.ANY, 9, 3, [0, 0, 0, 0, 0]),
+    (oracle.ANY, 3, 4, [0, 0, 0, 0, 1]),        # AND of all four models
+    (oracle.ANY, 5, 2, [1, 0, 0, 0, 0]),
+    (oracle.ANY, 8, 1, [0, 0, 0, 1, 0]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(POLICY_CASES)))
+def test_vote_policies_hand_worked(case):
+    policy, pos, k, want = POLICY_CASES[case]
+    assert oracle.vote_policy(POLICY_TOP1, 10, policy, pos, k).tolist() == want
+
+
+def test_plurality_is_the_smallest_mode():
+    # scipy.stats.mode returns the most frequent value, the smallest on ties
+    import scipy.stats
+    g = np.random.default_rng(5)
+    for N, C in [(1, 10), (2, 4), (3, 5), (5, 3), (7, 1000), (16, 6)]:
+        t = g.integers(0, C, size=(N, 200)).astype(np.int32)
+        want = scipy.stats.mode(t, axis=0, keepdims=False).mode
+        assert np.array_equal(oracle.vote_policy(t, C, oracle.PLURALITY), want), (N, C)
+
+
+def test_detection_policy_properties():
+    g = np.random.default_rng(6)
+    N, C = 5, 4
+    t = g.integers(0, C, size=(N, 300)).astype(np.int32)
+    for pos in range(C):
+        by_k = [oracle.vote_policy(t, C, oracle.ANY, pos, k) for k in range(1, N + 1)]
+        for a, b in zip(by_k, by_k[1:]):  # asking for more models never detects more
+            assert np.all(b <= a)
+        plural = oracle.vote_policy(t, C, oracle.PLURALITY)
+        assert np.all(by_k[0][plural == pos] == 1)  # the plurality class is named by someone
+    one = t[:1]  # a single model: plurality is its top-1, detection is top-1 == c*
+    assert np.array_equal(oracle.vote_policy(one, C, oracle.PLURALITY), one[0])
+    assert np.array_equal(oracle.vote_policy(one, C, oracle.ANY, 2, 1), (one[0] == 2).astype(np.int32))
+
+
 # -------------------------------------------------------------- whole nets
 def _torch_forward(layers, x, prec):
     """Independent float64 forward with torch CPU ops, rounding to the storage
