@@ -45,6 +45,11 @@ def parse():
                     help="launch every kernel of a step from the host instead of replaying the recorded pass")
     ap.add_argument("--combine", default="mean", choices=["mean", "plurality", "any"],
                     help="combine policy of vote (any: class 0 detected by at least one model)")
+    ap.add_argument("--serve", action="store_true",
+                    help="only time the request stream (200 requests of 1..64 ragged images, host "
+                         "images in, host results out): one client, 4 clients on shared handles, "
+                         "4 clients through one batcher; print one JSON line and exit")
+    ap.add_argument("--max-wait-us", type=int, default=500, help="batcher wait for --serve")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
@@ -99,8 +104,79 @@ def cpu_baseline(w, imgs, seconds):
                       f"({w['precision']} storage, double accumulation), {dt:.1f} s"}
 
 
+def serve_bench(args):
+    """Closed-loop request stream, end to end through fs_infer (PCIe
+    included): each client sends its next request when the last returned."""
+    import threading
+    import torch
+    import workloads as wl
+    from paper_2003_01538_amd import flexserve as fsb
+
+    torch.cuda.set_device(0)
+    sw = wl.STREAM_WORKLOAD
+    w = wl.workload(sw["ensemble"])
+    reqs = wl.request_stream(sw["seed"], sw["n_requests"], sw["sizes"], sw["lo"], sw["hi"])
+    n_img = sum(len(q) for q in reqs)
+    Bm, K = max(sw["sizes"]), 4
+    ens = fsb.Ensemble(w["models"], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"],
+                       max_batch=Bm)
+    handles = [ens] + [ens.share() for _ in range(K - 1)]
+    # tiles and graphs for every batch size a pass can see; the largest batch
+    # of the largest images first, so the staging buffers (part of a
+    # recorded pass's identity) never grow inside the timed loops
+    warm = [np.zeros((sw["hi"], sw["hi"], 3), np.uint8)] * Bm
+    for h in handles:
+        for b in [Bm] + list(range(1, Bm)):
+            h.infer(warm[:b], want_logits=False)
+
+    def run_clients(call):
+        errs = []
+
+        def client(k):
+            try:
+                for q in reqs[k::K]:
+                    call(k, q)
+            except Exception as ex:
+                errs.append(ex)
+        ts = [threading.Thread(target=client, args=(k,)) for k in range(K)]
+        t0 = time.perf_counter()
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        if errs:
+            raise errs[0]
+        return time.perf_counter() - t0
+
+    t0 = time.perf_counter()
+    for q in reqs:
+        ens.infer(q, want_logits=False)
+    seq_s = time.perf_counter() - t0
+    shared_s = run_clients(lambda k, q: handles[k].infer(q, want_logits=False))
+    res = {}
+    for nw in (1, 2, 4):  # one batcher worker per handle, all warmed above
+        with fsb.Batcher(handles[:nw], max_wait_us=args.max_wait_us) as bt:
+            t = run_clients(lambda k, q: bt.infer(q, want_logits=False))
+            res[nw] = dict(images_per_s=round(n_img / t, 1), passes=bt.stats()["passes"])
+    for h in handles:
+        h.close()
+    print(json.dumps({
+        "metric": "request-stream images/s (end to end, host images in, host results out)",
+        "unit": "images/s", "higher_is_better": True, "data": "synthetic: seeded uint8 noise images",
+        "config": {"workload": sw["name"], "requests": len(reqs), "images": n_img,
+                   "batch_sizes": list(sw["sizes"]), "image_hw": [sw["lo"], sw["hi"]], "max_batch": Bm},
+        "one_client": round(n_img / seq_s, 1),
+        "clients_4_shared_handles": round(n_img / shared_s, 1),
+        "clients_4_batcher": {f"workers_{k}": v for k, v in res.items()},
+        "batcher_max_wait_us": args.max_wait_us,
+    }))
+
+
 def main():
     args = parse()
+    if args.serve:
+        serve_bench(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported "
               "(every box has one GPU; the multi-GPU design is documented, not built)", file=sys.stderr)

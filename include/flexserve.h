@@ -124,6 +124,15 @@ typedef struct {
  * FS_ERR_DEVICE (no such device), FS_ERR_OOM. *out is NULL on failure. */
 fs_status fs_ensemble_create(const fs_ensemble_desc *desc, fs_ensemble **out);
 
+/* A second handle on the same ensemble (Sec. 2.2: several server workers
+ * serve one set of models): it shares src's device weights (no copy; they
+ * are freed with the last handle that uses them) and the plan, and has its
+ * own activation workspace, stream, lock, recorded graphs and combine
+ * policy, so calls on the two handles run concurrently.  src is not
+ * modified.  Errors: FS_ERR_INVALID (NULL), FS_ERR_DEVICE, FS_ERR_OOM; *out
+ * is NULL on failure. */
+fs_status fs_ensemble_share(fs_ensemble *src, fs_ensemble **out);
+
 /* Ensemble inference over a batch of B host images of any sizes (Sec. 2.3),
  * synchronous.  B == 0 is a no-op.  B > max_batch is processed in chunks.
  *   probs      [N][B][C] fp32, required
@@ -166,6 +175,33 @@ fs_status fs_graphs_enable(fs_ensemble *e, int32_t enable);
 fs_status fs_set_combine(fs_ensemble *e, int32_t policy, int32_t positive_class, int32_t min_votes);
 
 void fs_destroy(fs_ensemble *e); /* NULL-safe; waits for outstanding work */
+
+/* Request coalescing (Sec. 2.3: batches of any size per request).  A
+ * batcher serves fs_batcher_infer calls from any number of threads with one
+ * worker thread per handle in handles[0..n_handles) (1..16 handles of one
+ * ensemble: the first and handles shared from it with fs_ensemble_share).
+ * One worker at a time gathers: it takes queued requests whole, in arrival
+ * order, up to max_batch images per pass (a larger request runs alone,
+ * chunked by fs_infer), waiting up to max_wait_us after the first for
+ * others to arrive, and runs them as one fs_infer on its handle while the
+ * next worker gathers.  fs_batcher_infer has the arguments and output
+ * layout of fs_infer for its own B images and blocks until they are done;
+ * the caller's buffers must stay valid until it returns.  Each image's
+ * result is that of fs_infer on the same images in a batch of the pass's
+ * size.  The handles must outlive the batcher and may still be used
+ * directly.  FS_ERR_INVALID for NULL, n_handles outside 1..16, a negative
+ * wait, or handles whose models, classes, max_batch or weights differ.
+ * Errors are returned per call; their message is fs_batcher_last_error() of
+ * the calling thread. */
+typedef struct fs_batcher fs_batcher;
+fs_status fs_batcher_create(fs_ensemble *const *handles, int32_t n_handles, int32_t max_wait_us,
+                            fs_batcher **out);
+fs_status fs_batcher_infer(fs_batcher *b, const fs_image *imgs, int32_t B, float *probs,
+                           float *mean_probs, int32_t *vote, int32_t *top1, float *logits);
+/* Passes run, requests served and images served so far. */
+fs_status fs_batcher_stats(fs_batcher *b, int64_t *passes, int64_t *requests, int64_t *images);
+const char *fs_batcher_last_error(void);
+void fs_batcher_destroy(fs_batcher *b); /* NULL-safe; serves the queued requests first */
 
 /* Last error message of handle e, or of this thread's last failed create
  * when e is NULL.  Valid until the next call on the same handle/thread. */

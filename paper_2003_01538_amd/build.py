@@ -24,7 +24,7 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-function", "-I", INCLUDE, "-I", CSRC]
-SOURCES = ["runtime.cpp", "preprocess.hip", "conv.hip", "conv_dma.hip", "conv_hs.hip", "pool.hip", "fc.hip", "softmax.hip"]
+SOURCES = ["runtime.cpp", "batcher.cpp", "preprocess.hip", "conv.hip", "conv_dma.hip", "conv_hs.hip", "pool.hip", "fc.hip", "softmax.hip"]
 
 
 def _compile(src: str) -> str:

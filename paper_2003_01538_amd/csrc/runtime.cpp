@@ -61,9 +61,21 @@ float host_bf16_to_f(uint16_t h) {
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ------------------------------------------------------------ device memory
-struct DevBuf {
+struct DevBuf {  // owns one device allocation; movable, not copyable
   void* p = nullptr;
   size_t bytes = 0;
+  DevBuf() = default;
+  DevBuf(const DevBuf&) = delete;
+  DevBuf& operator=(const DevBuf&) = delete;
+  DevBuf(DevBuf&& o) noexcept : p(o.p), bytes(o.bytes) { o.p = nullptr; o.bytes = 0; }
+  DevBuf& operator=(DevBuf&& o) noexcept {
+    if (this != &o) {
+      release();
+      p = o.p; bytes = o.bytes;
+      o.p = nullptr; o.bytes = 0;
+    }
+    return *this;
+  }
   void alloc(size_t n) {
     release();
     if (n == 0) return;
@@ -81,9 +93,12 @@ struct DevBuf {
   ~DevBuf() { release(); }
 };
 
-struct HostBuf {  // pinned
+struct HostBuf {  // pinned; not copyable
   void* p = nullptr;
   size_t bytes = 0;
+  HostBuf() = default;
+  HostBuf(const HostBuf&) = delete;
+  HostBuf& operator=(const HostBuf&) = delete;
   void ensure(size_t n) {
     if (n <= bytes) return;
     release();
@@ -155,7 +170,8 @@ struct fs_ensemble {
   fs_preprocess pre{};
   std::vector<Group> groups;
   double flops_per_image = 0;
-  DevBuf arena;
+  // weights, shared by every handle made from this one with fs_ensemble_share
+  std::shared_ptr<DevBuf> arena = std::make_shared<DevBuf>();
   size_t arena_bytes = 0;
   DevBuf input;     // [max_batch][out_h][out_w][4]
   DevBuf input_s2d; // [max_batch][out_h/2][out_w/2][16] bf16
@@ -514,6 +530,9 @@ void set_device(int dev) {
   HIPCHK(hipSetDevice(dev));
 }
 
+void alloc_workspace(fs_ensemble* e);
+ConvArgs conv_args(fs_ensemble* e, Group& g, const LayerPlan& P, int B, void* y, int64_t y_ms);
+
 void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   e->prec = d->precision == FS_BF16 ? BF16 : F32;
   e->N = d->num_models;
@@ -577,9 +596,15 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   set_device(e->device);
   e->num_cus = num_cus_of(e->device);
   HIPCHK(hipStreamCreateWithFlags(&e->stream, hipStreamNonBlocking));
-  e->arena.alloc(std::max<size_t>(off, 256));
-  HIPCHK(hipMemcpy(e->arena.p, host.data(), off, hipMemcpyHostToDevice));
+  e->arena->alloc(std::max<size_t>(off, 256));
+  HIPCHK(hipMemcpy(e->arena->p, host.data(), off, hipMemcpyHostToDevice));
+  alloc_workspace(e);
+}
 
+// Activation slots, split-K scratch, transformed-input and logit buffers of
+// one handle, for its max_batch.
+void alloc_workspace(fs_ensemble* e) {
+  const size_t esz = es(e->prec);
   const int Bm = e->max_batch;
   int64_t ws = 0;
   for (Group& g : e->groups) {
@@ -599,6 +624,16 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
         for (int B = 1; B <= Bm; ++B)
           pf_all = std::max(pf_all, fc_partial_floats(B, P.out.C, fc_pick_split(e->prec, B, P.K, P.out.C, g.Z, e->num_cus), g.Z));
   e->partial.alloc(round_up(std::max<size_t>(pf_all, 1) * 4, 256));
+  // split-K scratch of the conv layers, likewise for every batch size: a
+  // layer's K split grows as its M shrinks, so a batch below its bucket's
+  // size can need more than the bucket size itself
+  size_t cf_all = 0;
+  for (Group& g : e->groups)
+    for (LayerPlan& P : g.layers)
+      if (P.op == FS_OP_CONV && !P.pool_fused)
+        for (int B = 1; B <= Bm; ++B) cf_all = std::max(cf_all, conv_partial_floats(conv_args(e, g, P, B, nullptr, 0)));
+  if (cf_all) e->conv_partial.alloc(round_up(cf_all * 4, 256));
+  ws += e->conv_partial.bytes;
   if (e->need_plain) e->input.alloc(round_up((size_t)Bm * e->pre.out_h * e->pre.out_w * 4 * esz, 256));
   if (e->need_s2d) e->input_s2d.alloc(round_up((size_t)Bm * e->pre.out_h * e->pre.out_w * 4 * 2, 256));
   e->logits.alloc(round_up((size_t)e->N * Bm * e->C * 4, 256));
@@ -649,7 +684,7 @@ void* slot_ptr(Group& g, int slot) { return g.slots[slot].p; }
 
 ConvArgs conv_args(fs_ensemble* e, Group& g, const LayerPlan& P, int B, void* y, int64_t y_ms) {
   const int Bm = e->max_batch;
-  char* arena = static_cast<char*>(e->arena.p);
+  char* arena = static_cast<char*>(e->arena->p);
   ConvArgs a{};
   a.x = P.in_slot == SLOT_INPUT ? (P.s2d ? e->input_s2d.p : e->input.p) : slot_ptr(g, P.in_slot);
   a.x_mstride = P.in_slot == SLOT_INPUT ? 0 : (int64_t)g.slot_elems[P.in_slot] * Bm;
@@ -758,7 +793,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
   launch(K_PRE, 0.0, (double)B * oh * ow * 3 * esz * ((e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0)),
          (e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0), [&] { launch_preprocess(pa, p, s); });
 
-  char* arena = static_cast<char*>(e->arena.p);
+  char* arena = static_cast<char*>(e->arena->p);
   const std::vector<std::vector<int>>& tiles = tiles_for(e, B, s);
   for (size_t gi = 0; gi < e->groups.size(); ++gi) {
     Group& g = e->groups[gi];
@@ -787,6 +822,8 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
       switch (P.op) {
         case FS_OP_CONV: {
           const ConvArgs a = conv_args(e, g, P, B, y, y_ms);
+          if (conv_partial_floats(a) * 4 > e->conv_partial.bytes)  // sized at create for every B
+            fail(FS_ERR_INTERNAL, "split-K scratch too small for this batch size");
           const int tile = tiles[gi][li];
           launch.M = a.M; launch.N = a.Cout; launch.K = P.kreal;
           launch.kernel = P.pool_fused ? "stem_s2d_conv_maxpool" : conv_tile(p, tile).name;
@@ -1066,6 +1103,51 @@ fs_status fs_ensemble_create(const fs_ensemble_desc* desc, fs_ensemble** out) {
     e = new fs_ensemble();
     try {
       build(e, desc);
+    } catch (...) {
+      destroy_impl(e);
+      e = nullptr;
+      throw;
+    }
+  });
+  if (st == FS_OK) *out = e;
+  return st;
+}
+
+fs_status fs_ensemble_share(fs_ensemble* src, fs_ensemble** out) {
+  if (out) *out = nullptr;
+  if (!src || !out) {
+    g_thread_error = "ensemble or out is NULL";
+    return FS_ERR_INVALID;
+  }
+  fs_ensemble* e = nullptr;
+  fs_status st = guarded(nullptr, [&] {
+    std::lock_guard<std::mutex> lk(src->mu);
+    e = new fs_ensemble();
+    try {
+      e->device = src->device;
+      e->num_cus = src->num_cus;
+      e->prec = src->prec;
+      e->N = src->N; e->C = src->C; e->max_batch = src->max_batch;
+      e->combine = src->combine; e->pos_class = src->pos_class; e->min_votes = src->min_votes;
+      e->pre = src->pre;
+      e->groups.resize(src->groups.size());
+      for (size_t i = 0; i < src->groups.size(); ++i) {  // the plan; slots are the new handle's own
+        e->groups[i].first = src->groups[i].first;
+        e->groups[i].Z = src->groups[i].Z;
+        e->groups[i].layers = src->groups[i].layers;
+        e->groups[i].slot_elems = src->groups[i].slot_elems;
+      }
+      e->flops_per_image = src->flops_per_image;
+      e->arena = src->arena;
+      e->arena_bytes = src->arena_bytes;
+      e->need_plain = src->need_plain;
+      e->need_s2d = src->need_s2d;
+      e->tiles = src->tiles;
+      e->tune = src->tune;
+      e->graphs = src->graphs;
+      set_device(e->device);
+      HIPCHK(hipStreamCreateWithFlags(&e->stream, hipStreamNonBlocking));
+      alloc_workspace(e);
     } catch (...) {
       destroy_impl(e);
       e = nullptr;

@@ -99,6 +99,15 @@ SIGNATURES = [
     ("fs_profile_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
     ("fs_graphs_enable", ctypes.c_int, [_vp, ctypes.c_int32]),
     ("fs_set_combine", ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    ("fs_ensemble_share", ctypes.c_int, [_vp, ctypes.POINTER(_vp)]),
+    ("fs_batcher_create", ctypes.c_int, [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.POINTER(_vp)]),
+    ("fs_batcher_infer", ctypes.c_int, [_vp, ctypes.POINTER(fs_image), ctypes.c_int32, _fp, _fp, _i32p, _i32p,
+                                        _fp]),
+    ("fs_batcher_stats", ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_int64)]),
+    ("fs_batcher_last_error", ctypes.c_char_p, []),
+    ("fs_batcher_destroy", None, [_vp]),
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
     ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
@@ -278,6 +287,48 @@ def fs_graphs_enable(handle, enable=True):
     _check(load().fs_graphs_enable(handle, int(bool(enable))), handle)
 
 
+def fs_ensemble_share(handle) -> int:
+    h = _vp()
+    _check(load().fs_ensemble_share(handle, ctypes.byref(h)))
+    return h.value
+
+
+def _check_batcher(st):
+    if st != FS_OK:
+        m = load().fs_batcher_last_error()
+        raise FsError(st, m.decode() if m else "")
+
+
+def fs_batcher_create(handles, max_wait_us=2000) -> int:
+    arr = (_vp * len(handles))(*handles)
+    b = _vp()
+    _check_batcher(load().fs_batcher_create(arr, len(handles), int(max_wait_us), ctypes.byref(b)))
+    return b.value
+
+
+def fs_batcher_infer(batcher, imgs, N, C, want_mean=True, want_top1=True, want_logits=False):
+    B = len(imgs)
+    probs = np.zeros((N, B, C), np.float32)
+    mean = np.zeros((B, C), np.float32) if want_mean else None
+    vote = np.zeros(B, np.int32)
+    top1 = np.zeros((N, B), np.int32) if want_top1 else None
+    logits = np.zeros((N, B, C), np.float32) if want_logits else None
+    arr, keep = image_array(imgs)
+    _check_batcher(load().fs_batcher_infer(batcher, arr, B, _f(probs), _f(mean), _i(vote), _i(top1),
+                                           _f(logits)))
+    return dict(probs=probs, mean=mean, vote=vote, top1=top1, logits=logits)
+
+
+def fs_batcher_stats(batcher) -> dict:
+    p, r, i = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check_batcher(load().fs_batcher_stats(batcher, ctypes.byref(p), ctypes.byref(r), ctypes.byref(i)))
+    return dict(passes=p.value, requests=r.value, images=i.value)
+
+
+def fs_batcher_destroy(batcher):
+    load().fs_batcher_destroy(batcher)
+
+
 def fs_set_combine(handle, policy, positive_class=0, min_votes=1):
     _check(load().fs_set_combine(handle, int(policy), int(positive_class), int(min_votes)), handle)
 
@@ -437,6 +488,13 @@ class Ensemble:
     def set_combine(self, policy, positive_class=0, min_votes=1):
         fs_set_combine(self.handle, policy, positive_class, min_votes)
 
+    def share(self):
+        """A second handle on the same device weights (fs_ensemble_share)."""
+        other = Ensemble.__new__(Ensemble)
+        other.handle = fs_ensemble_share(self.handle)
+        other.N, other.C = self.N, self.C
+        return other
+
     def close(self):
         if self.handle:
             fs_destroy(self.handle)
@@ -447,6 +505,32 @@ class Ensemble:
             self.close()
         except Exception:
             pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+
+class Batcher:
+    """Request coalescing over handles of one ensemble (fs_batcher_*): one
+    worker per Ensemble given (the first and handles from its share())."""
+
+    def __init__(self, ens, max_wait_us=2000):
+        self.handles = list(ens) if isinstance(ens, (list, tuple)) else [ens]  # must outlive the batcher
+        self.b = fs_batcher_create([h.handle for h in self.handles], max_wait_us)
+
+    def infer(self, imgs, **kw):
+        return fs_batcher_infer(self.b, imgs, self.handles[0].N, self.handles[0].C, **kw)
+
+    def stats(self):
+        return fs_batcher_stats(self.b)
+
+    def close(self):
+        if self.b:
+            fs_batcher_destroy(self.b)
+            self.b = None
 
     def __enter__(self):
         return self

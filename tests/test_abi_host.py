@@ -105,6 +105,7 @@ def test_create_rejects_null_and_empty():
 
 
 def test_calls_on_null_handle_fail_cleanly():
+    import ctypes
     lib = fsb.load()
     assert lib.fs_infer(None, None, 0, None, None, None, None, None) == fsb.FS_ERR_INVALID
     assert lib.fs_infer_device(None, None, None, 1, None, None, None, None, None, None) == fsb.FS_ERR_INVALID
@@ -112,6 +113,17 @@ def test_calls_on_null_handle_fail_cleanly():
     assert lib.fs_profile_enable(None, 1) == fsb.FS_ERR_INVALID
     assert lib.fs_graphs_enable(None, 1) == fsb.FS_ERR_INVALID
     assert lib.fs_set_combine(None, fsb.FS_COMBINE_PLURALITY, 0, 1) == fsb.FS_ERR_INVALID
+    h = ctypes.c_void_p(1)
+    assert lib.fs_ensemble_share(None, ctypes.byref(h)) == fsb.FS_ERR_INVALID and not h.value
+    b = ctypes.c_void_p(1)
+    assert lib.fs_batcher_create(None, 1, 100, ctypes.byref(b)) == fsb.FS_ERR_INVALID and not b.value
+    nulls = (ctypes.c_void_p * 2)()
+    assert lib.fs_batcher_create(nulls, 2, 100, ctypes.byref(b)) == fsb.FS_ERR_INVALID and not b.value
+    assert lib.fs_batcher_create(nulls, 0, 100, ctypes.byref(b)) == fsb.FS_ERR_INVALID
+    assert lib.fs_batcher_infer(None, None, 1, None, None, None, None, None) == fsb.FS_ERR_INVALID
+    assert lib.fs_batcher_stats(None, None, None, None) == fsb.FS_ERR_INVALID
+    assert lib.fs_batcher_last_error()
+    lib.fs_batcher_destroy(None)
     lib.fs_destroy(None)
 
 

@@ -226,3 +226,139 @@ def test_combine_policies_per_call(wname):
                       combine=fsb.FS_COMBINE_PLURALITY) as ens:
         g = ens.infer(imgs)
         assert np.array_equal(g["vote"], oracle.vote_policy(g["top1"], C, fsb.FS_COMBINE_PLURALITY))
+
+
+def test_shared_handles_run_concurrently():
+    # Two handles on one set of device weights serve two threads at once,
+    # each with its own workspace and stream; every result has the bits of
+    # the single-handle pass, and the weights outlive the handle that
+    # created them.
+    import threading
+    w = wl.workload("resnet18x3_bf16_b32")
+    imgs = _images(w)
+    ens = _ensemble(w, max_batch=32)
+    other = None
+    try:
+        ref_a, ref_b = ens.infer(imgs[:16]), ens.infer(imgs[16:])
+        other = ens.share()
+        assert other.info()["weight_bytes"] == ens.info()["weight_bytes"]
+        out, errs = {}, []
+
+        def work(h, key, part):
+            try:
+                for i in range(4):
+                    out[(key, i)] = h.infer(part)
+            except Exception as ex:  # reported below
+                errs.append(ex)
+
+        ts = [threading.Thread(target=work, args=(ens, "a", imgs[:16])),
+              threading.Thread(target=work, args=(other, "b", imgs[16:]))]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        assert not errs, errs
+        for i in range(4):
+            for k in ("probs", "logits", "vote", "top1", "mean"):
+                assert np.array_equal(out[("a", i)][k], ref_a[k]), (i, k)
+                assert np.array_equal(out[("b", i)][k], ref_b[k]), (i, k)
+        other.set_combine(fsb.FS_COMBINE_PLURALITY)  # a handle's policy is its own
+        assert np.array_equal(ens.infer(imgs[16:])["vote"], ref_b["vote"])
+        ens.close()
+        g = other.infer(imgs[:16])
+        assert np.array_equal(g["probs"], ref_a["probs"])
+        assert np.array_equal(g["vote"], oracle.vote_policy(g["top1"], g["probs"].shape[2], fsb.FS_COMBINE_PLURALITY))
+    finally:
+        ens.close()
+        if other is not None:
+            other.close()
+
+
+def test_batcher_coalesces_concurrent_requests():
+    # Four clients' requests (5 + 11 + 3 + 13 = max_batch images) run as one
+    # pass and each gets the bits of its images in a batch of 32; with no
+    # wait, requests pass through one by one; a request above max_batch runs
+    # alone, chunked; a bad request fails alone.
+    import threading
+    w = wl.workload("resnet18x3_bf16_b32")
+    imgs = _images(w)
+    with _ensemble(w, max_batch=32) as ens:
+        ref = ens.infer(imgs)
+        sizes, parts, o = [5, 11, 3, 13], [], 0
+        for s in sizes:
+            parts.append((o, imgs[o:o + s]))
+            o += s
+        res, errs = {}, []
+        with fsb.Batcher(ens, max_wait_us=10_000_000) as bt:
+            def client(k):
+                try:
+                    res[k] = bt.infer(parts[k][1], want_logits=True)
+                except Exception as ex:
+                    errs.append(ex)
+            ts = [threading.Thread(target=client, args=(k,)) for k in range(len(parts))]
+            for t in ts:
+                t.start()
+            for t in ts:
+                t.join()
+            assert not errs, errs
+            assert bt.stats() == dict(passes=1, requests=4, images=32)
+        for k, (o, part) in enumerate(parts):
+            b = len(part)
+            for key in ("probs", "logits"):
+                assert np.array_equal(res[k][key], ref[key][:, o:o + b]), (k, key)
+            assert np.array_equal(res[k]["top1"], ref["top1"][:, o:o + b])
+            assert np.array_equal(res[k]["vote"], ref["vote"][o:o + b])
+            assert np.array_equal(res[k]["mean"], ref["mean"][o:o + b])
+        with fsb.Batcher(ens, max_wait_us=0) as b0:
+            for q in (imgs[:7], imgs[7:8], imgs + imgs[:8]):
+                g, r = b0.infer(q), ens.infer(q)
+                for key in ("probs", "vote", "top1", "mean"):
+                    assert np.array_equal(g[key], r[key]), (len(q), key)
+            assert b0.stats() == dict(passes=3, requests=3, images=48)
+            with pytest.raises(fsb.FsError) as e:
+                b0.infer([imgs[0], np.zeros((0, 4, 3), np.uint8)])
+            assert e.value.status == fsb.FS_ERR_INVALID
+            assert b0.stats()["requests"] == 3
+        # two workers on two handles of the ensemble: full-batch requests from
+        # four clients, each pass a batch of 32 whatever the arrival order
+        other = ens.share()
+        try:
+            perms = [np.random.default_rng(k).permutation(32) for k in range(4)]
+            qs = [[imgs[i] for i in p] for p in perms]
+            refs = [ens.infer(q) for q in qs]
+            res2, errs = {}, []
+            with fsb.Batcher([ens, other], max_wait_us=1000) as b2:
+                def client2(k):
+                    try:
+                        for _ in range(3):
+                            res2.setdefault(k, []).append(b2.infer(qs[k]))
+                    except Exception as ex:
+                        errs.append(ex)
+                ts = [threading.Thread(target=client2, args=(k,)) for k in range(4)]
+                for t in ts:
+                    t.start()
+                for t in ts:
+                    t.join()
+                assert not errs, errs
+                assert b2.stats() == dict(passes=12, requests=12, images=384)
+            for k in range(4):
+                for g in res2[k]:
+                    for key in ("probs", "vote", "top1", "mean"):
+                        assert np.array_equal(g[key], refs[k][key]), (k, key)
+        finally:
+            other.close()
+
+
+def test_batch_sizes_inside_a_bucket():
+    # Tiles are planned per power-of-two bucket of batch sizes, but a conv
+    # layer's K split grows as the batch shrinks: layer4's first conv of
+    # ResNet-18 splits at B = 33..48 and not at B = 64, so the split-K
+    # scratch must cover every batch size, not just the bucket's own.
+    w = wl.workload("resnet18x3_bf16_b32")
+    s = wl.STREAM_WORKLOAD
+    q = [im for r in wl.request_stream(s["seed"], 8) for im in r]
+    while len(q) < 64:
+        q = q + q
+    with _ensemble(w, max_batch=64) as ens:
+        for B in (17, 33, 40, 63):
+            _check(w, ens, q[:B], [0, B - 1])
