@@ -362,3 +362,57 @@ def test_batch_sizes_inside_a_bucket():
     with _ensemble(w, max_batch=64) as ens:
         for B in (17, 33, 40, 63):
             _check(w, ens, q[:B], [0, B - 1])
+
+
+def test_http_front_end():
+    # POSTs from concurrent clients are answered with every model's classes
+    # and the combined result of the library on the same images; bad
+    # requests get 400.
+    import base64
+    import json
+    import threading
+    import urllib.error
+    import urllib.request
+    from paper_2003_01538_amd import serve
+    w = wl.workload("tiny2_fp32_b4")
+    rng = np.random.default_rng(9)
+    reqs = [[rng.integers(0, 256, size=(int(rng.integers(20, 60)), int(rng.integers(20, 60)), 3), dtype=np.uint8)
+             for _ in range(n)] for n in (1, 3, 2, 4, 6)]
+    ens = _ensemble(w)
+    other = ens.share()
+    try:
+        refs = [ens.infer(q) for q in reqs]
+        with serve.Server([ens, other], max_wait_us=2000, policy="plurality") as srv:
+            def post(obj):
+                r = urllib.request.Request(srv.url + "/infer", data=json.dumps(obj).encode(),
+                                           headers={"Content-Type": "application/json"})
+                with urllib.request.urlopen(r, timeout=60) as f:
+                    return json.loads(f.read())
+            with urllib.request.urlopen(srv.url + "/health", timeout=60) as f:
+                assert json.loads(f.read()) == {"models": 2, "classes": 10, "max_batch": 4, "policy": "plurality"}
+            got, errs = {}, []
+
+            def client(k):
+                try:
+                    arrs = [{"shape": list(a.shape), "data": base64.b64encode(a.tobytes()).decode()} for a in reqs[k]]
+                    got[k] = post({"arrays": arrs})
+                except Exception as ex:
+                    errs.append(ex)
+            ts = [threading.Thread(target=client, args=(k,)) for k in range(len(reqs))]
+            for t in ts:
+                t.start()
+            for t in ts:
+                t.join()
+            assert not errs, errs
+            for k, ref in enumerate(refs):
+                for i in range(2):
+                    assert got[k][f"model y_{i}"] == ref["top1"][i].tolist()
+                assert got[k]["combined"] == oracle.vote_policy(ref["top1"], 10, fsb.FS_COMBINE_PLURALITY).tolist()
+            for bad in ({"arrays": []}, {"images": ["!!"]},
+                        {"policy": "mean", "arrays": [{"shape": [1, 1, 3], "data": "AAAA"}]}):
+                with pytest.raises(urllib.error.HTTPError) as e:
+                    post(bad)
+                assert e.value.code == 400
+    finally:
+        other.close()
+        ens.close()
