@@ -317,6 +317,9 @@ static const ConvTile kTilesBF16[] = {
     {256, 64, 8, "bf16dma2_256x64_w4m4_v8", 2, 4, 4},
     {224, 64, 8, "bf16halo_4x56_n64_v8", 0, 7, 7, 1, 4, 56},
     {128, 128, 8, "bf16hs_128x128_w4_v8", 0, 4, 2, 2},
+    {128, 128, 8, "bf16dma1_128x128_w4_v8", 1, 4, 2},
+    {128, 64, 8, "bf16dma1_128x64_w4_v8", 1, 4, 2},
+    {64, 128, 8, "bf16dma1_64x128_w4_v8", 1, 4, 2},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},

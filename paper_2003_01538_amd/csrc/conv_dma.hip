@@ -213,7 +213,7 @@ __device__ __forceinline__ TileCoord tile_coord(const ConvArgs& a, int bid) {
 // of 32), v_mfma_f32_32x32x16_bf16.
 template <int BM, int BN, int WGM, int WGN, int STAGES>
 __global__ void __launch_bounds__(64 * WGM * WGN,
-                                  (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
+                                  STAGES == 1 ? 4 : (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
   constexpr int NW = WGM * WGN;
   constexpr int TM = BM / WGM, TN = BN / WGN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -309,16 +309,29 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   // this workgroup's share of the K-tiles (all of them unless split-K)
   const int nk_all = a.Kp / BK;
   const int kb = sp * nk_all / a.split, nk = (sp + 1) * nk_all / a.split - kb;
+  if constexpr (STAGES == 1) {
+    // one buffer (for layers of one or a few K-tiles, where a deeper ring
+    // only costs occupancy): fetch, wait, compute, and meet again before the
+    // next fetch overwrites the buffer
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt > 0) __builtin_amdgcn_s_barrier();
+      issue(kb + kt, 0);
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      compute(0);
+    }
+  } else {
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(kb + s, s);
-  for (int kt = 0; kt < nk; ++kt) {
-    // tiles issued after kt that may stay in flight
-    const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
-    wait_tiles<STAGES - 2, LPT>(ahead);
-    __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < nk) issue(kb + kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    compute(kt % STAGES);
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) issue(kb + s, s);
+    for (int kt = 0; kt < nk; ++kt) {
+      // tiles issued after kt that may stay in flight
+      const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
+      wait_tiles<STAGES - 2, LPT>(ahead);
+      __builtin_amdgcn_s_barrier();
+      if (kt + STAGES - 1 < nk) issue(kb + kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+      compute(kt % STAGES);
+    }
   }
 
   conv_epilogue<FM, FN>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane);
@@ -1023,6 +1036,9 @@ void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int 
   FS_DMA(128, 64, 2, 2, 2)
   FS_DMA(64, 128, 2, 2, 2)
   FS_DMA(256, 64, 4, 1, 2)
+  FS_DMA(128, 128, 2, 2, 1)
+  FS_DMA(128, 64, 2, 2, 1)
+  FS_DMA(64, 128, 2, 2, 1)
 #undef FS_DMA
 }
 
