@@ -68,10 +68,14 @@ def test_preprocess_parity(gpu_lib, prec, case):
 
 def test_preprocess_space_to_depth_layout(gpu_lib):
     rng = np.random.default_rng(4001)
-    # ragged sizes, a square image, a strided view and a very wide image
+    # ragged sizes, a square image, a strided view, a very wide image (its
+    # taps gathered through the cache), tiny images, and the widest rows the
+    # kernel stages in LDS (511 pixels) next to the narrowest it does not (512)
     big = rng.integers(0, 256, (300, 420, 3), dtype=np.uint8)
     imgs = (wl.images_ragged(4000, 3) + [wl.images_uniform(5, 1, 224, 224)[0]]
-            + [big[7:290, 11:400], rng.integers(0, 256, (37, 1500, 3), dtype=np.uint8)])
+            + [big[7:290, 11:400], rng.integers(0, 256, (37, 1500, 3), dtype=np.uint8)]
+            + [rng.integers(0, 256, (1, 1, 3), dtype=np.uint8), rng.integers(0, 256, (3, 5, 3), dtype=np.uint8),
+               rng.integers(0, 256, (20, 511, 3), dtype=np.uint8), rng.integers(0, 256, (21, 512, 3), dtype=np.uint8)])
     g = fsb.fs_test_preprocess(imgs, 224, 224, MEAN, STD, BF16, layout=1)
     assert g.shape == (len(imgs), 112, 112, 16) and np.all(g[..., 12:] == 0)
     for i, im in enumerate(imgs):
