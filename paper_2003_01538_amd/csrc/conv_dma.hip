@@ -716,11 +716,11 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
   const __amdgpu_buffer_rsrc_t ry = rsrc(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride,
                                          (uint32_t)((int64_t)a.B * Hp * Wp * 64 * 2));
 
-  // the two pooled rows of step ps (whose activated rows are in the ring)
-  auto pool_step = [&](int ps, bool live_step) {
+  // item u of this thread's share of the two pooled rows of step ps (whose
+  // activated rows are in the ring): one 16-byte store, written or dropped
+  auto pool_item = [&](int ps, bool live_step, int u) {
     const int b = step_img(ps), rho0 = step_rho(ps);
-#pragma unroll
-    for (int u = 0; u < STEM_NSTORE; ++u) {
+    {
       const int item = tid + u * 64 * STEM_WAVES;
       const int q = item / (Wp * 8), rest = item - q * (Wp * 8);
       const int px = rest >> 3, ch = rest & 7;
@@ -740,9 +740,14 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
           }
         }
       }
-      const uint32_t off = live ? (uint32_t)(((((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) * 2) : OOB;
+      const uint32_t off = live ? (uint32_t)(((((int64_t)b * Hp + py) * Wp + px) * 64 + ch * 8) * 2)
+                                : OOB + 16u * (uint32_t)u;  // distinct: never merged
       __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, m), ry, off, 0, 0);
     }
+  };
+  auto pool_step = [&](int ps, bool live_step) {
+#pragma unroll
+    for (int u = 0; u < STEM_NSTORE; ++u) pool_item(ps, live_step, u);
   };
 
   auto do_step = [&](int st, const char* Pb, char* Pn) __attribute__((always_inline)) {
@@ -758,10 +763,20 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    // the previous step's pooled rows are interleaved with these MFMAs: they
+    // read only the ring, so their LDS reads, maxima and stores issue while
+    // the matrix cores work
+    const int pps = st > 0 ? st - 1 : 0;
+    const bool plive = st > 0 && st - 1 >= carry;
 #pragma unroll
     for (int ky = 0; ky < 4; ++ky) {
 #pragma unroll
       for (int kx = 0; kx < 4; ++kx) {
+        constexpr int NTAP = 16;
+        const int tap = ky * 4 + kx;
+#pragma unroll
+        for (int u = 0; u < STEM_NSTORE; ++u)
+          if (tap == (u + 1) * NTAP / (STEM_NSTORE + 1)) pool_item(pps, plive, u);
         bf16x8 af[STEM_FM], bfr[2];
 #pragma unroll
         for (int i = 0; i < STEM_FM; ++i)
@@ -776,8 +791,6 @@ __global__ void __launch_bounds__(64 * STEM_WAVES, 1) k_stem_pool(ConvArgs a) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
       }
     }
-    // the previous step's pooled rows, while these MFMAs run
-    pool_step(st > 0 ? st - 1 : 0, st > 0 && st - 1 >= carry);
     wait_lgkm0();
     wg_barrier();  // the ring rows the pooling read may now be overwritten
     // activated bf16 conv rows into the LDS ring (row rho in buffer rho % 5)
