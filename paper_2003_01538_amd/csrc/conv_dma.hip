@@ -372,7 +372,7 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane >> 3, fr = lane & 31, fq = lane >> 5;
-  const int CH = a.Cin / BK, nkt = a.Kp / BK;
+  const int nkt = a.Kp / BK;
 
   // ---- this workgroup's group (model z, N-tile) and range of spatial tiles
   const int tiles_h = (a.Ho + TH - 1) / TH, T = a.B * tiles_h;
@@ -403,11 +403,17 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
     }
   }
 
-  // ---- patch loads: pixel q of the patch is input (oy0 - 1 + q / PW, q % PW - 1)
-  int q_dy[NIT], q_ix[NIT], q_lc[NIT];
+  // ---- patch loads: pixel q of the patch is input (oy0 - 1 + q / PW, q % PW - 1).
+  // Every wave issues NIT instructions for every patch (a wave past the last
+  // block repeats it: the same bytes to the same LDS slot), the step after the
+  // last fetches out of range, and the residual loads are unconditional, so
+  // each wave's count of vector-memory operations is the same on every path
+  // and the compiler's own waits are exact rather than full drains.
+  int q_dy[NIT], q_ix[NIT], q_lc[NIT], q_blk[NIT];
 #pragma unroll
   for (int it = 0; it < NIT; ++it) {
-    const int blk = it * NW + wave;
+    const int blk = min(it * NW + wave, NPB - 1);
+    q_blk[it] = blk;
     const int q = blk * 8 + lr;
     q_lc[it] = (lane & 7) ^ (((q / PW * TW + q % PW) >> 1) & 7);
     if (blk < NPB && q < NP) {
@@ -419,19 +425,18 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
       q_ix[it] = 0;
     }
   }
-  auto issue_patch = [&](int t, int cc, int buf) {
+  auto issue_patch = [&](int t, int cc, int buf, bool live) {
     const int img = t / tiles_h, oy0 = (t - img * tiles_h) * TH;
     char* pb = psm + buf * PATCH;
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
-      const int blk = it * NW + wave;
-      if (blk < NPB) {
-        const int iy = oy0 + q_dy[it], ix = q_ix[it];
-        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-        const uint32_t off =
-            ok ? (uint32_t)(((((int64_t)img * a.H + iy) * a.W + ix) * a.Cin + cc * BK + q_lc[it] * 8) * 2) : OOB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + blk * 1024), 16, off, 0, 0, 0);
-      }
+      const int iy = oy0 + q_dy[it], ix = q_ix[it];
+      const bool ok = live && (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+      const uint32_t keep = 0u - (uint32_t)ok;  // a bitwise blend keeps the load unconditional
+      const uint32_t real =
+          (uint32_t)(((((int64_t)img * a.H + max(iy, 0)) * a.W + max(ix, 0)) * a.Cin + cc * BK + q_lc[it] * 8) * 2);
+      const uint32_t off = (real & keep) | (OOB & ~keep);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + q_blk[it] * 1024), 16, off, 0, 0, 0);
     }
   };
 
@@ -461,7 +466,11 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
         bias_v[j][h][4] = b1.x; bias_v[j][h][5] = b1.y; bias_v[j][h][6] = b1.z; bias_v[j][h][7] = b1.w;
       }
   }
-  const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
+  const bool has_res = a.res != nullptr;
+  // residual through a buffer resource (empty without one: every load reads zero)
+  const __amdgpu_buffer_rsrc_t rres =
+      has_res ? rsrc(reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride, (uint32_t)((int64_t)a.M * a.Cout * 2))
+              : rsrc(a.y, 0u);
 
   floatx16 acc[FM][FN];
   auto zero_acc = [&]() {
@@ -473,8 +482,11 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   };
   zero_acc();
-  uint4 res_v[FM][FN][2];
-  int mg[FM];
+  // Two register sets for the tiles' output rows and residuals: a step uses
+  // one and fetches the next tile's into the other, so no copy (which the
+  // compiler guarded with a full wait) moves them between steps.
+  uint4 res_a[FM][FN][2], res_b[FM][FN][2];
+  int mg_a[FM], mg_b[FM];
 
   // outputs through a buffer resource: an epilogue issues exactly NSTORE
   // stores per lane (out-of-range ones are dropped), so the next step waits
@@ -482,41 +494,49 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
   constexpr int NSTORE = FM * FN * 2;
   const __amdgpu_buffer_rsrc_t ry = rsrc(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride,
                                          (uint32_t)((int64_t)a.M * a.Cout * 2));
-  const int steps = (t_end - t_begin) * CH;
-  issue_patch(t_begin, 0, 0);
-  // every step ends with NSTORE stores (dropped ones where no tile ends), so
-  // every step starts with the same count of stores in flight behind its patch
-  dummy_stores<NSTORE>(ry);
-  for (int st = 0; st < steps; ++st) {
-    const int tj = st / CH, cc = st - tj * CH;
-    wait_vmcnt<NSTORE>();  // the patch landed; the last step's stores may be in flight
-    wg_barrier();
-    if (cc == CH - 1) {  // the tile's output rows and residual, requested before the next patch
-      const int t = t_begin + tj;
-      const int img = t / tiles_h, oy0 = (t - img * tiles_h) * TH;
+  // a tile's output rows and its residual (into rv), fetched one tile ahead,
+  // behind the next tile's patch: the wait for that patch also covers it
+  auto tile_rows_res = [&](int t, int (&m_)[FM], uint4 (&rv)[FM][FN][2]) {
+    const int img = t / tiles_h, oy0 = (t - img * tiles_h) * TH;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int oy = oy0 + pr_[i];
-        mg[i] = oy < a.Ho ? (img * a.Ho + oy) * a.Wo + pc_[i] : -1;
+    for (int i = 0; i < FM; ++i) {
+      const int oy = oy0 + pr_[i];
+      m_[i] = oy < a.Ho ? (img * a.Ho + oy) * a.Wo + pc_[i] : -1;
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int n = n0 + j * 32 + 8 * (2 * h + fq);
-            res_v[i][j][h] = (res && mg[i] >= 0) ? *reinterpret_cast<const uint4*>(res + (int64_t)mg[i] * a.Cout + n)
-                                                  : uint4{0, 0, 0, 0};
-          }
-      }
+        for (int h = 0; h < 2; ++h) {
+          const int n = n0 + j * 32 + 8 * (2 * h + fq);
+          // a bitwise blend, not a select: the compiler turned the select into
+          // two branches with a load each, which made the load count vary
+          const uint32_t keep = 0u - (uint32_t)(m_[i] >= 0);
+          const uint32_t off = ((uint32_t)((max(m_[i], 0) * a.Cout + n) * 2) & keep) |
+                               ((OOB + 16u * (uint32_t)((i * FN + j) * 2 + h)) & ~keep);  // distinct: never merged
+          rv[i][j][h] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rres, off, 0, 0));
+        }
     }
-    if (st + 1 < steps) {
-      const int tn = (st + 1) / CH;
-      issue_patch(t_begin + tn, st + 1 - tn * CH, (st + 1) & 1);
+  };
+  // One 64-channel chunk (conv_halo_ok: the resident weights hold at most
+  // 9 x 64 x BN), so a step is a whole tile.
+  const int steps = t_end - t_begin;
+  issue_patch(t_begin, 0, 0, true);
+  tile_rows_res(t_begin, mg_a, res_a);
+  dummy_stores<NSTORE>(ry);  // every step starts with NSTORE stores in flight behind its patch
+  auto step = [&](int st, const int (&mg)[FM], const uint4 (&res_v)[FM][FN][2], int (&mg_n)[FM],
+                  uint4 (&res_n)[FM][FN][2]) {
+    wait_vmcnt<NSTORE>();  // the patch and the tile's residual landed; the last step's stores may be in flight
+    wg_barrier();
+    {  // the next tile's patch (out of range after the last tile) and residual
+      const bool live = st + 1 < steps;
+      const int tn = t_begin + min(st + 1, steps - 1);
+      issue_patch(tn, 0, (st + 1) & 1, live);
+      tile_rows_res(tn, mg_n, res_n);
+      __builtin_amdgcn_sched_barrier(0);  // issued here, not sunk among the MFMAs: they have the whole step to land
     }
     const char* Pb = psm + (st & 1) * PATCH;
 #pragma unroll
     for (int tap = 0; tap < 9; ++tap) {
       const int ky = tap / 3, kx = tap - ky * 3;
-      const int kt = tap * CH + cc;
       int ra[FM], sa[FM], rb[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
@@ -524,45 +544,48 @@ __global__ void __launch_bounds__(64 * (TH * TW / 32) / FM, 1) k_conv_halo(ConvA
         sa[i] = ((h0[i] + ky * TW + kx) >> 1) & 7;
       }
 #pragma unroll
-      for (int j = 0; j < FN; ++j) rb[j] = kt * BN + j * 32 + fr;
+      for (int j = 0; j < FN; ++j) rb[j] = tap * BN + j * 32 + fr;
       mma_ktile_rows_sw<FM, FN>(Pb, wsm, ra, sa, rb, lane, acc);
     }
-    if (cc != CH - 1) {
-      dummy_stores<NSTORE>(ry);
-    } else {  // epilogue: bias, residual, ReLU, bf16, 16-byte stores
+    // epilogue: bias, residual, ReLU, bf16, 16-byte stores
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int gp = 2 * h;
-            float v[8], rr[8];
+        for (int h = 0; h < 2; ++h) {
+          const int gp = 2 * h;
+          float v[8], rr[8];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
-                                                               __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
-              v[r] = __uint_as_float(sw[0]);
-              v[4 + r] = __uint_as_float(sw[1]);
-            }
-#pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] += bias_v[j][h][e];
-            if (res) {
-              bf8_to_f8(res_v[i][j][h], rr);
-#pragma unroll
-              for (int e = 0; e < 8; ++e) v[e] += rr[e];
-            }
-            if (a.relu)
-#pragma unroll
-              for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
-            const int n = n0 + j * 32 + 8 * (gp + fq);
-            const uint32_t off = mg[i] >= 0 ? (uint32_t)(((int64_t)mg[i] * a.Cout + n) * 2)
-                                            : OOB + 16u * (uint32_t)((i * FN + j) * 2 + h);  // distinct: never merged
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry, off, 0, 0);
+          for (int r = 0; r < 4; ++r) {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][gp * 4 + r]),
+                                                             __float_as_uint(acc[i][j][(gp + 1) * 4 + r]), false, false);
+            v[r] = __uint_as_float(sw[0]);
+            v[4 + r] = __uint_as_float(sw[1]);
           }
-      zero_acc();
-    }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += bias_v[j][h][e];
+          if (has_res) {
+            bf8_to_f8(res_v[i][j][h], rr);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += rr[e];
+          }
+          if (a.relu)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+          const int n = n0 + j * 32 + 8 * (gp + fq);
+          const uint32_t keep = 0u - (uint32_t)(mg[i] >= 0);
+          const uint32_t off = ((uint32_t)((max(mg[i], 0) * a.Cout + n) * 2) & keep) |
+                               ((OOB + 16u * (uint32_t)((i * FN + j) * 2 + h)) & ~keep);  // distinct: never merged
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry, off, 0, 0);
+        }
+    zero_acc();
+  };
+  for (int st = 0; st < steps; st += 2) {
+    step(st, mg_a, res_a, mg_b, res_b);
+    if (st + 1 < steps) step(st + 1, mg_b, res_b, mg_a, res_a);
   }
+  wait_vmcnt<0>();  // the out-of-range fetches after the last step land before the workgroup leaves
 }
 
 // The ResNet stem fused: 7x7/2 conv in its space-to-depth form (4x4/1,
@@ -989,7 +1012,7 @@ bool conv_dma_ok(const ConvArgs& a) {
 constexpr int HALO_WBYTES = 72 * 1024;
 
 bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn) {
-  return a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin % BK == 0 && a.K == a.Kp &&
+  return a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin == BK && a.K == a.Kp &&
          a.Wo == tw && a.Ho == a.H && a.Wo == a.W && a.Cout % bn == 0 && a.split == 1 &&
          (int64_t)a.Kp * bn * 2 <= HALO_WBYTES && a.Z * (a.Cout / bn) <= 4096;
 }
