@@ -216,7 +216,11 @@ def main():
     d_mean = torch.empty((B, C), dtype=torch.float32, device="cuda")
     d_vote = torch.empty(B, dtype=torch.int32, device="cuda")
     d_top1 = torch.empty((N, B), dtype=torch.int32, device="cuda")
-    stream = torch.cuda.current_stream()
+    # a stream of our own: the pass runs on it, so events recorded on it
+    # bracket the whole pass (stream 0 would hand the pass to the library's
+    # own stream)
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
 
     def step():
         fsb.fs_infer_device(ens.handle, d_pix.data_ptr(), d_desc.data_ptr(), B, d_probs.data_ptr(),
@@ -267,6 +271,37 @@ def main():
                                               share=v["total_ms"] / args.steps / (plain_s / args.steps * 1e3))
                                       for k, v in stats.items()}}), file=sys.stderr)
 
+    # per-step spread of the device-resident pass, events on the launch stream
+    spans = []
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(args.steps):
+        ev0.record(stream)
+        step()
+        ev1.record(stream)
+        ev1.synchronize()
+        spans.append(ev0.elapsed_time(ev1))
+    spans = np.sort(np.asarray(spans))
+    # end to end: host uint8 images in, host results out (PCIe included; never the value)
+    walls = []
+    for i in range(max(3, args.steps // 5) + 2):
+        t0 = time.perf_counter()
+        ens.infer(imgs, want_logits=False)
+        if i >= 2:
+            walls.append((time.perf_counter() - t0) * 1e3)
+    walls = np.sort(np.asarray(walls))
+
+    def pct(v):
+        return {q: round(float(np.percentile(v, p)), 4) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))}
+
+    hbm = None
+    if stats:
+        # memory-bound kernel classes: algorithmic bytes over their event time
+        hbm = {k: {"achieved": round(v["bytes"] / (v["total_ms"] * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+                   "unit": "GB/s", "frac": round(v["bytes"] / (v["total_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                   "avg_us": round(v["total_ms"] / v["launches"] * 1e3, 2)}
+               for k, v in stats.items() if k in ("preprocess", "maxpool", "gap", "fc", "softmax_combine")
+               and v["launches"] > 0 and v["total_ms"] > 0}
+
     ms = plain_s / args.steps * 1e3
     out = {
         "metric": "ensemble images/sec at B=32 (3xResNet-18, bf16) + MFMA util vs peak",
@@ -283,6 +318,10 @@ def main():
                    "flops_per_image": info["flops_per_image"],
                    "launches_per_step": info["launches_per_pass"]},
         "roofline": roof,
+        "hbm_kernels": hbm,
+        "device_step_ms": pct(spans),
+        "end_to_end": {"images_per_s": round(B / float(np.median(walls)) * 1e3, 1), "ms": pct(walls),
+                       "note": "fs_infer from host images to host results, PCIe included"},
     }
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(w, imgs, args.cpu_seconds)
