@@ -23,6 +23,7 @@ struct PreArgs {
   const ImageDesc* desc;
   int B, out_h, out_w;
   float mean[3], std_[3];
+  float inv_std[3];  // 1 / std_, set by launch_preprocess
   void* out;      // [B][out_h][out_w][4], bf16 or fp32, or null
   void* out_s2d;  // bf16 [B][out_h/2][out_w/2][16] space-to-depth layout, or null:
                   // channel (sy*2 + sx)*3 + c holds pixel (2Y+sy, 2X+sx), channel c;
