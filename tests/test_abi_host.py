@@ -162,3 +162,19 @@ def test_test_entries_validate_before_device():
     assert e.value.status == fsb.FS_ERR_UNSUPPORTED
     assert lib.fs_conv_num_tiles(fsb.FS_BF16) >= 3 and lib.fs_conv_num_tiles(9) == 0
     assert fsb.fs_conv_tile_name(fsb.FS_BF16, 0) and fsb.fs_conv_tile_name(fsb.FS_BF16, 99) is None
+
+
+@pytest.mark.parametrize("out", [1, 9, 17, 112, 224, 1000, 4096])
+def test_float_reciprocal_quotient_is_exact_below_2_pow_22(out):
+    # The preprocess kernel takes floor(n / d), d = 2 * out, as
+    # trunc((n + 0.5) * fl(1/d)) in fp32 when n + 1 < 2^22, and the fraction
+    # as (n - q d) * fl(1/d).  Every such n, in fp32 arithmetic as on the
+    # device, gives the integer quotient; the fraction is within 2 ulps.
+    d = 2 * out
+    n = np.arange(1, (1 << 22) - 1, dtype=np.int64)
+    inv = np.float32(1.0) / np.float32(d)
+    q = ((n.astype(np.float32) + np.float32(0.5)) * inv).astype(np.int64)
+    assert np.array_equal(q, n // d)
+    frac = (n - q * d).astype(np.float32) * inv
+    exact = (n % d) / d
+    assert np.all(np.abs(frac.astype(np.float64) - exact) <= 2 * np.spacing(np.float32(1.0)) * np.maximum(exact, 1e-30) + 1e-12)
