@@ -283,7 +283,7 @@ def main():
     spans = np.sort(np.asarray(spans))
     # end to end: host uint8 images in, host results out (PCIe included; never the value)
     walls = []
-    for i in range(max(3, args.steps // 5) + 2):
+    for i in range(max(10, args.steps // 2) + 2):
         t0 = time.perf_counter()
         ens.infer(imgs, want_logits=False)
         if i >= 2:

@@ -15,13 +15,16 @@
 
 #include <algorithm>
 #include <cmath>
+#include <condition_variable>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <memory>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 namespace {
@@ -160,6 +163,76 @@ struct ProfRec {
 
 }  // namespace
 
+namespace fs {
+namespace {
+
+// Helper threads for the host side of fs_infer: copying the caller's images
+// into the pinned staging buffer (several MB at B = 32) is its largest host
+// cost.  run(n, f) calls f(0) .. f(n - 1), each once, spread over the
+// helpers and the calling thread, and returns when all have returned; f must
+// not throw.  One run at a time (the ensemble's lock is held).
+class HostPool {
+ public:
+  explicit HostPool(int helpers) {
+    try {
+      for (int i = 0; i < helpers; ++i) th_.emplace_back([this] { work(); });
+    } catch (...) {  // fewer helpers (or none): the caller does the rest
+    }
+  }
+  ~HostPool() {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      stop_ = true;
+    }
+    go_.notify_all();
+    for (std::thread& t : th_) t.join();
+  }
+  void run(int n, const std::function<void(int)>& f) {
+    std::unique_lock<std::mutex> lk(mu_);
+    job_ = &f;
+    parts_ = n;
+    next_ = done_ = 0;
+    ++gen_;
+    go_.notify_all();
+    take(lk);
+    done_cv_.wait(lk, [&] { return done_ == parts_; });
+    job_ = nullptr;
+    parts_ = next_ = done_ = 0;
+  }
+
+ private:
+  void take(std::unique_lock<std::mutex>& lk) {
+    while (next_ < parts_) {
+      const int i = next_++;
+      const std::function<void(int)>* f = job_;
+      lk.unlock();
+      (*f)(i);
+      lk.lock();
+      if (++done_ == parts_) done_cv_.notify_all();
+    }
+  }
+  void work() {
+    std::unique_lock<std::mutex> lk(mu_);
+    uint64_t seen = 0;
+    for (;;) {
+      go_.wait(lk, [&] { return stop_ || (gen_ != seen && next_ < parts_); });
+      if (stop_) return;
+      seen = gen_;
+      take(lk);
+    }
+  }
+  std::vector<std::thread> th_;
+  std::mutex mu_;
+  std::condition_variable go_, done_cv_;
+  const std::function<void(int)>* job_ = nullptr;
+  int parts_ = 0, next_ = 0, done_ = 0;
+  uint64_t gen_ = 0;
+  bool stop_ = false;
+};
+
+}  // namespace
+}  // namespace fs
+
 struct fs_ensemble {
   std::mutex mu;
   std::string err;
@@ -182,6 +255,7 @@ struct fs_ensemble {
   // host-path staging
   DevBuf d_pixels, d_desc, d_probs, d_mean, d_vote, d_top1;
   HostBuf h_pixels, h_desc, h_out;
+  std::unique_ptr<fs::HostPool> pack_pool;  // started by the first fs_infer
   hipStream_t stream = nullptr;
   // conv tile per (batch bucket) -> per group -> per layer, measured once
   std::map<int, std::vector<std::vector<int>>> tiles;
@@ -1089,6 +1163,56 @@ void pack_images(const fs_image* imgs, int b0, int nb, uint8_t* dst, ImageDesc* 
   }
 }
 
+// The same packing, staged for an overlapped upload: descriptors first, then
+// the bytes in `pieces` parts of about equal size, each copied by the pool
+// (in units of at most ~256 KB: whole images, or row blocks of a large one)
+// and handed to `piece_done(begin, end)` (a byte range of dst) before the
+// next part is copied.  A contiguous image (row_stride = 3w) is one memcpy.
+void pack_images_staged(const fs_image* imgs, int b0, int nb, uint8_t* dst, ImageDesc* desc, HostPool& pool,
+                        int pieces, const std::function<void(size_t, size_t)>& piece_done) {
+  struct Unit {
+    int b, y0, y1;
+  };
+  size_t off = 0;
+  for (int b = b0; b < b0 + nb; ++b) {
+    const fs_image& im = imgs[b];
+    const size_t row = (size_t)im.w * 3;
+    desc[b - b0] = ImageDesc{off, im.h, im.w, (int32_t)row, 0};
+    off += round_up(row * im.h, 16);
+  }
+  const size_t total = off;
+  constexpr size_t UNIT = 256 << 10;
+  std::vector<Unit> units;
+  int b = b0;
+  size_t done = 0;  // bytes of dst handed over so far
+  for (int p = 0; p < pieces && b < b0 + nb; ++p) {
+    // whole images up to this piece's share of the bytes (at least one)
+    const size_t goal = total * (size_t)(p + 1) / (size_t)pieces;
+    units.clear();
+    do {
+      const fs_image& im = imgs[b];
+      const size_t row = (size_t)im.w * 3;
+      const int rows = (int)std::max<size_t>(1, UNIT / row);
+      for (int y = 0; y < im.h; y += rows) units.push_back(Unit{b, y, std::min(im.h, y + rows)});
+      ++b;
+    } while (b < b0 + nb && desc[b - b0].offset < goal);
+    pool.run((int)units.size(), [&](int u) {
+      const Unit& t = units[u];
+      const fs_image& im = imgs[t.b];
+      const size_t row = (size_t)im.w * 3;
+      uint8_t* d = dst + desc[t.b - b0].offset + (size_t)t.y0 * row;
+      if ((size_t)im.row_stride == row) {
+        std::memcpy(d, im.data + (size_t)t.y0 * row, (size_t)(t.y1 - t.y0) * row);
+      } else {
+        for (int y = t.y0; y < t.y1; ++y) std::memcpy(d + (size_t)(y - t.y0) * row, im.data + (size_t)y * im.row_stride, row);
+      }
+    });
+    const size_t end = b < b0 + nb ? (size_t)desc[b - b0].offset : total;
+    piece_done(done, end);
+    done = end;
+  }
+}
+
 }  // namespace
 
 // ==================================================================== ABI
@@ -1204,8 +1328,16 @@ fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs
       e->h_pixels.ensure(pbytes);
       e->d_pixels.ensure(pbytes);
       ImageDesc* hd = static_cast<ImageDesc*>(e->h_desc.p);
-      pack_images(imgs, b0, nb, static_cast<uint8_t*>(e->h_pixels.p), hd);
-      HIPCHK(hipMemcpyAsync(e->d_pixels.p, e->h_pixels.p, pbytes, hipMemcpyHostToDevice, s));
+      if (!e->pack_pool) {
+        const unsigned hw = std::thread::hardware_concurrency();
+        e->pack_pool = std::make_unique<HostPool>((int)std::min(3u, hw > 1 ? hw - 1 : 0u));
+      }
+      // the first part's upload overlaps the copying of the second
+      uint8_t* hpix = static_cast<uint8_t*>(e->h_pixels.p);
+      uint8_t* dpix = static_cast<uint8_t*>(e->d_pixels.p);
+      pack_images_staged(imgs, b0, nb, hpix, hd, *e->pack_pool, 2, [&](size_t lo, size_t hi) {
+        if (hi > lo) HIPCHK(hipMemcpyAsync(dpix + lo, hpix + lo, hi - lo, hipMemcpyHostToDevice, s));
+      });
       HIPCHK(hipMemcpyAsync(e->d_desc.p, hd, nb * sizeof(ImageDesc), hipMemcpyHostToDevice, s));
       float* dlog = static_cast<float*>(e->logits.p);
       run_pass_cached(e, static_cast<const uint8_t*>(e->d_pixels.p), static_cast<const ImageDesc*>(e->d_desc.p),

@@ -143,6 +143,28 @@ def test_determinism_permutation_and_device_path():
                                 0, d_vote.data_ptr(), 0, 0, stream.cuda_stream)
 
 
+def test_host_staging_of_strided_large_and_tiny_images():
+    # fs_infer copies the caller's images into pinned memory in parts (whole
+    # images, or row blocks of a large one, over several threads) and uploads
+    # the first part while the second is copied.  Strided views, an image
+    # larger than one copy unit, tiny images and two chunks give the bits of
+    # the same images passed as contiguous arrays, and the oracle's values.
+    w = wl.workload("tiny2_fp32_b4")
+    rng = np.random.default_rng(77)
+    base = rng.integers(0, 256, (120, 900, 3), dtype=np.uint8)
+    imgs = [base[3:110, 5:700], rng.integers(0, 256, (700, 420, 3), dtype=np.uint8),
+            rng.integers(0, 256, (1, 1, 3), dtype=np.uint8), rng.integers(0, 256, (3, 5, 3), dtype=np.uint8)]
+    imgs += wl.images_ragged(9, 6, 20, 48) + [base[::2, 100:300]]
+    assert imgs[0].strides[0] != 3 * imgs[0].shape[1] and imgs[-1].strides[0] != 3 * imgs[-1].shape[1]
+    with _ensemble(dict(w, batch=8), max_batch=8) as ens:
+        g = ens.infer(imgs)
+        gc = ens.infer([np.ascontiguousarray(im) for im in imgs])
+        for k in ("probs", "logits", "vote", "top1", "mean"):
+            assert np.array_equal(g[k], gc[k]), k
+        o = oracle.ensemble(w["models"], imgs, w["out_hw"], MEAN, STD, "fp32")
+        compare(g, o, "fp32")
+
+
 def test_chunked_batches_and_empty_batch():
     w = wl.workload("tiny2_fp32_b4")
     imgs = wl.images_ragged(5, 11, 20, 48)
