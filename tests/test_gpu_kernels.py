@@ -85,6 +85,26 @@ def test_preprocess_space_to_depth_layout(gpu_lib):
         assert_bf16_close(g[i, ..., :12], r, frac_exact=0.99, what=f"s2d[{i}]", abs_tol=2e-6)
 
 
+@pytest.mark.parametrize("layout", [0, 1])
+def test_preprocess_tap_division_fallback(gpu_lib, layout):
+    # Tap positions come from a float reciprocal while 2 * out * in < 2^22
+    # and from integer division beyond; 224 outputs from more than 9362
+    # input pixels along an axis take the integer path (rows and columns).
+    rng = np.random.default_rng(4002)
+    imgs = [rng.integers(0, 256, (3, 12000, 3), dtype=np.uint8), rng.integers(0, 256, (12000, 2, 3), dtype=np.uint8),
+            rng.integers(0, 256, (9400, 9, 3), dtype=np.uint8), rng.integers(0, 256, (40, 60, 3), dtype=np.uint8)]
+    prec = BF16
+    g = fsb.fs_test_preprocess(imgs, 224, 224, MEAN, STD, prec, layout=layout)
+    for i, im in enumerate(imgs):
+        o = oracle.preprocess(im, 224, 224, MEAN, STD, "bf16")
+        if layout == 1:
+            o = o.reshape(112, 2, 112, 2, 3).transpose(0, 2, 1, 3, 4).reshape(112, 112, 12)
+            got = g[i, ..., :12]
+        else:
+            got = g[i, ..., :3]
+        assert_bf16_close(got, o, frac_exact=0.99, what=f"fallback[{layout}][{i}]", abs_tol=2e-6)
+
+
 # ----------------------------------------------------------------------- conv
 CONV_CASES = [
     # B, H, W, Cin, Cout, k, stride, pad, relu, residual
