@@ -143,7 +143,14 @@ void fs_batcher::run(Worker& wk) {
     gathering = false;
     cv_work.notify_all();  // the next worker may gather
     lk.unlock();
-    pass(wk, batch);
+    try {
+      pass(wk, batch);
+    } catch (...) {  // host buffers of the pass could not grow: the requests fail, the worker lives on
+      for (Request* r : batch) {
+        r->st = FS_ERR_OOM;
+        r->err = "batcher: host allocation failed";
+      }
+    }
     lk.lock();
     ++passes;
     requests += (int64_t)batch.size();
@@ -238,7 +245,12 @@ fs_status fs_batcher_infer(fs_batcher* b, const fs_image* imgs, int32_t B, float
       g_batcher_error = "batcher is shutting down";
       return FS_ERR_INVALID;
     }
-    b->queue.push_back(&r);
+    try {
+      b->queue.push_back(&r);
+    } catch (...) {
+      g_batcher_error = "batcher: host allocation failed";
+      return FS_ERR_OOM;
+    }
     b->queued_images += B;
     b->cv_work.notify_all();  // the gathering worker re-checks its fill
     b->cv_done.wait(lk, [&] { return r.done; });
