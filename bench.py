@@ -41,8 +41,9 @@ def parse():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (scales the HBM byte "
                          "counters of a profiler run) and exit")
-    ap.add_argument("--no-graphs", action="store_true",
-                    help="launch every kernel of a step from the host instead of replaying the recorded pass")
+    ap.add_argument("--graphs", action="store_true",
+                    help="record each step's launches once and replay them (fs_graphs_enable) instead of "
+                         "launching every kernel from the host (the default, measured faster)")
     ap.add_argument("--combine", default="mean", choices=["mean", "plurality", "any"],
                     help="combine policy of vote (any: class 0 detected by at least one model)")
     ap.add_argument("--serve", action="store_true",
@@ -200,8 +201,8 @@ def main():
     imgs = list(wl.images_uniform(w["image_seed"], B, *w["in_hw"]))
     ens = fsb.Ensemble(w["models"], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"],
                        max_batch=B)
-    if args.no_graphs:
-        fsb.fs_graphs_enable(ens.handle, False)
+    if args.graphs:
+        fsb.fs_graphs_enable(ens.handle, True)
     if args.combine != "mean":
         policy = {"plurality": fsb.FS_COMBINE_PLURALITY, "any": fsb.FS_COMBINE_ANY}[args.combine]
         fsb.fs_set_combine(ens.handle, policy, 0, 1)

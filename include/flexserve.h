@@ -156,13 +156,17 @@ fs_status fs_infer_device(fs_ensemble *e, const uint8_t *d_pixels,
                           float *d_probs, float *d_mean_probs, int32_t *d_vote,
                           int32_t *d_top1, float *d_logits, void *stream);
 
-/* HIP graphs for the pass (on by default).  fs_infer and fs_infer_device
- * record the pass's kernel launches the first time a batch size meets a set
- * of buffers on a stream and replay them with one launch from then on
- * (the scheduler row of the hot path: one graph per exact batch size).  The
- * pass runs eagerly while the profiler is on and on the legacy default
- * stream.  enable = 0 turns graphs off and drops the recorded passes.
- * Synchronises the ensemble's stream.  FS_ERR_INVALID for a NULL handle. */
+/* HIP graphs for the pass (off by default).  With enable = 1, fs_infer and
+ * fs_infer_device record the pass's kernel launches the first time a batch
+ * size meets a set of buffers on a stream and replay them with one launch
+ * from then on (one graph per exact batch size).  Off, every kernel is
+ * launched from the host; the host then stays far ahead of the device
+ * (25 launches against a pass of 0.27 ms or more for three ResNet-18s), and
+ * replay measured 0.7-2 % slower per pass at every batch size from 1 to 32,
+ * so graphs are for callers that need one launch per pass.  The pass runs
+ * eagerly while the profiler is on and on the legacy default stream.
+ * enable = 0 drops the recorded passes.  Synchronises the ensemble's
+ * stream.  FS_ERR_INVALID for a NULL handle. */
 fs_status fs_graphs_enable(fs_ensemble *e, int32_t enable);
 
 /* Combine policy of the following fs_infer / fs_infer_device calls

@@ -261,8 +261,9 @@ struct fs_ensemble {
   std::map<int, std::vector<std::vector<int>>> tiles;
   bool tune = true;
   // captured passes, replayed with one launch: key = batch size, stream and
-  // every buffer the pass reads or writes (caller's and the ensemble's own)
-  bool graphs = true;
+  // every buffer the pass reads or writes (caller's and the ensemble's own);
+  // off by default (eager launches measured faster, see fs_graphs_enable)
+  bool graphs = false;
   std::map<std::vector<uintptr_t>, hipGraphExec_t> graph_cache;
   // profiler
   bool prof_on = false;
