@@ -122,9 +122,9 @@ def serve_bench(args):
     ens = fsb.Ensemble(w["models"], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"],
                        max_batch=Bm)
     handles = [ens] + [ens.share() for _ in range(K - 1)]
-    # tiles and graphs for every batch size a pass can see; the largest batch
-    # of the largest images first, so the staging buffers (part of a
-    # recorded pass's identity) never grow inside the timed loops
+    # conv tiles for every batch size a pass can see, timed before the clock
+    # starts; the largest batch of the largest images first, so the pinned
+    # staging buffers reach their final size here, not inside the timed loops
     warm = [np.zeros((sw["hi"], sw["hi"], 3), np.uint8)] * Bm
     for h in handles:
         for b in [Bm] + list(range(1, Bm)):
