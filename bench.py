@@ -50,7 +50,7 @@ def parse():
                     help="only time the request stream (200 requests of 1..64 ragged images, host "
                          "images in, host results out): one client, 4 clients on shared handles, "
                          "4 clients through one batcher; print one JSON line and exit")
-    ap.add_argument("--max-wait-us", type=int, default=500, help="batcher wait for --serve")
+    ap.add_argument("--max-wait-us", type=int, default=100, help="batcher wait for --serve")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
