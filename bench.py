@@ -51,6 +51,9 @@ def parse():
                          "images in, host results out): one client, 4 clients on shared handles, "
                          "4 clients through one batcher; print one JSON line and exit")
     ap.add_argument("--max-wait-us", type=int, default=100, help="batcher wait for --serve")
+    ap.add_argument("--no-e2e", action="store_true",
+                    help="skip the end-to-end fs_infer timing (host images in, host results out), so that "
+                         "only device-resident passes run, as in a kernel-trace profile")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
     return ap.parse_args()
@@ -284,7 +287,7 @@ def main():
     spans = np.sort(np.asarray(spans))
     # end to end: host uint8 images in, host results out (PCIe included; never the value)
     walls = []
-    for i in range(max(10, args.steps // 2) + 2):
+    for i in range(0 if args.no_e2e else max(10, args.steps // 2) + 2):
         t0 = time.perf_counter()
         ens.infer(imgs, want_logits=False)
         if i >= 2:
@@ -321,8 +324,9 @@ def main():
         "roofline": roof,
         "hbm_kernels": hbm,
         "device_step_ms": pct(spans),
-        "end_to_end": {"images_per_s": round(B / float(np.median(walls)) * 1e3, 1), "ms": pct(walls),
-                       "note": "fs_infer from host images to host results, PCIe included"},
+        "end_to_end": None if args.no_e2e else {
+            "images_per_s": round(B / float(np.median(walls)) * 1e3, 1), "ms": pct(walls),
+            "note": "fs_infer from host images to host results, PCIe included"},
     }
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(w, imgs, args.cpu_seconds)
