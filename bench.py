@@ -270,6 +270,24 @@ def main():
                 "algorithmic_bytes_per_launch": round(sum(r["bytes"] for r in conv) / len(conv)),
                 "kernel": "conv layer (implicit-GEMM dispatch + split-K reduce where used), mean over the layers of a step",
                 "avg_launch_us": round(per_launch_ms * 1e3, 2)}
+        # per conv layer: achieved rate against the peak and against the
+        # attainable min(peak, AI x HBM bandwidth), AI = algorithmic FLOP per
+        # algorithmic HBM byte (the 1x1 downsamples sit far below the ridge)
+        by_layer = {}
+        for r in conv:
+            by_layer.setdefault((r["group"], r["layer"]), []).append(r)
+        conv_layers = []
+        for (gi, li), rs in sorted(by_layer.items()):
+            ms_l = sum(r["ms"] for r in rs) / len(rs)
+            fl, by = rs[0]["flops"], rs[0]["bytes"]
+            tf = fl / (ms_l * 1e-3) / 1e12
+            ai = fl / by
+            att = min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
+            conv_layers.append({"layer": li, "kernel": rs[0]["kernel"], "MNK": [rs[0]["M"], rs[0]["N"], rs[0]["K"]],
+                                "us": round(ms_l * 1e3, 2), "tflops": round(tf, 1), "ai": round(ai, 1),
+                                "attainable": round(att, 1), "frac_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                                "frac_attainable": round(tf / att, 4)})
+        roof["conv_layers"] = conv_layers
         print(json.dumps({"profiled_ms_per_step": prof_s / args.steps * 1e3,
                           "kernels": {k: dict(v, avg_us=v["total_ms"] / v["launches"] * 1e3,
                                               share=v["total_ms"] / args.steps / (plain_s / args.steps * 1e3))
