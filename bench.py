@@ -103,9 +103,24 @@ def cpu_baseline(w, imgs, seconds):
         if time.perf_counter() - t0 >= seconds:
             break
     dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "images/s", "cores": omp_threads(), "kind": "oracle",
-            "sample": f"{n} of the {len(imgs)} images through all {len(w['models'])} models "
-                      f"({w['precision']} storage, double accumulation), {dt:.1f} s"}
+    out = {"value": n / dt, "unit": "images/s", "cores": omp_threads(), "kind": "oracle",
+           "sample": f"{n} of the {len(imgs)} images through all {len(w['models'])} models "
+                     f"({w['precision']} storage, double accumulation), {dt:.1f} s"}
+    # the same oracle on one thread, one image (its sums do not depend on the thread count)
+    try:
+        gomp = ctypes.CDLL("libgomp.so.1")
+    except OSError:
+        return out
+    threads = gomp.omp_get_max_threads()
+    gomp.omp_set_num_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.ensemble(w["models"], imgs[:1], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"], prepared)
+        dt1 = time.perf_counter() - t0
+    finally:
+        gomp.omp_set_num_threads(threads)
+    out["single_thread"] = {"value": 1 / dt1, "unit": "images/s", "cores": 1, "sample": f"1 image, {dt1:.1f} s"}
+    return out
 
 
 def serve_bench(args):
