@@ -25,6 +25,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 (the fp32 convs run on fp32 MFMA)
+DEFAULT_WORKLOAD = "resnet18x3_bf16_b32"
+METRIC = "ensemble images/sec at B=32 (3xResNet-18, bf16) + MFMA util vs peak"
 PEAK_HBM_GBS = 8000.0
 
 
@@ -33,7 +36,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="resnet18x3_bf16_b32")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    help="tiny2_fp32_b4, resnet18x3_bf16_b32 (the headline), hetero_r18_r50_vgg11_bf16_b32, "
+                         "resnet50x5_bf16_b256")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="bound on the CPU-oracle sample (0 disables it)")
     ap.add_argument("--dump-launches", default="",
@@ -91,21 +96,33 @@ def omp_threads():
         return os.cpu_count()
 
 
-def cpu_baseline(w, imgs, seconds):
+def _oracle_rate(w, imgs, prec, seconds):
+    """Images/s of the oracle over a bounded sample of imgs (all models)."""
     import oracle
     import workloads as wl
-    prepared = [oracle.prepare_model(m, w["precision"]) for m in w["models"]]
+    prepared = [oracle.prepare_model(m, prec) for m in w["models"]]
     n, t0 = 0, time.perf_counter()
     while n < len(imgs):
-        oracle.ensemble(w["models"], imgs[n:n + 1], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD,
-                        w["precision"], prepared)
+        oracle.ensemble(w["models"], imgs[n:n + 1], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, prec, prepared)
         n += 1
         if time.perf_counter() - t0 >= seconds:
             break
     dt = time.perf_counter() - t0
-    out = {"value": n / dt, "unit": "images/s", "cores": omp_threads(), "kind": "oracle",
-           "sample": f"{n} of the {len(imgs)} images through all {len(w['models'])} models "
-                     f"({w['precision']} storage, double accumulation), {dt:.1f} s"}
+    return n / dt, (f"{n} of the {len(imgs)} images through all {len(w['models'])} models "
+                    f"({prec} storage, double accumulation), {dt:.1f} s"), prepared
+
+
+def cpu_baseline(w, imgs, seconds):
+    """The oracle on this host's cores: fp32 storage (the reported value) and,
+    for a bf16 workload, its bf16-storage emulation alongside; plus fp32 on
+    one thread for one image."""
+    import oracle
+    import workloads as wl
+    v, sample, prepared = _oracle_rate(w, imgs, "fp32", seconds)
+    out = {"value": v, "unit": "images/s", "cores": omp_threads(), "kind": "oracle", "sample": sample}
+    if w["precision"] == "bf16":
+        vb, sb, _ = _oracle_rate(w, imgs, "bf16", seconds / 2)
+        out["bf16_storage"] = {"value": vb, "unit": "images/s", "cores": omp_threads(), "sample": sb}
     # the same oracle on one thread, one image (its sums do not depend on the thread count)
     try:
         gomp = ctypes.CDLL("libgomp.so.1")
@@ -115,11 +132,12 @@ def cpu_baseline(w, imgs, seconds):
     gomp.omp_set_num_threads(1)
     try:
         t0 = time.perf_counter()
-        oracle.ensemble(w["models"], imgs[:1], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"], prepared)
+        oracle.ensemble(w["models"], imgs[:1], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, "fp32", prepared)
         dt1 = time.perf_counter() - t0
     finally:
         gomp.omp_set_num_threads(threads)
-    out["single_thread"] = {"value": 1 / dt1, "unit": "images/s", "cores": 1, "sample": f"1 image, {dt1:.1f} s"}
+    out["single_thread"] = {"value": 1 / dt1, "unit": "images/s", "cores": 1,
+                            "sample": f"1 image, fp32 storage, {dt1:.1f} s"}
     return out
 
 
@@ -167,16 +185,30 @@ def serve_bench(args):
             raise errs[0]
         return time.perf_counter() - t0
 
+    def pct(v):
+        v = np.asarray(v)
+        return {"p50": round(float(np.percentile(v, 50)), 3), "p99": round(float(np.percentile(v, 99)), 3)}
+
+    lat = []
     t0 = time.perf_counter()
     for q in reqs:
+        t1 = time.perf_counter()
         ens.infer(q, want_logits=False)
+        lat.append((time.perf_counter() - t1) * 1e3)
     seq_s = time.perf_counter() - t0
-    shared_s = run_clients(lambda k, q: handles[k].infer(q, want_logits=False))
+    lat_sh = []
+
+    def timed(fn, k, q, out):
+        t1 = time.perf_counter()
+        fn(k, q)
+        out.append((time.perf_counter() - t1) * 1e3)
+    shared_s = run_clients(lambda k, q: timed(lambda k_, q_: handles[k_].infer(q_, want_logits=False), k, q, lat_sh))
     res = {}
     for nw in (1, 2, 4):  # one batcher worker per handle, all warmed above
         with fsb.Batcher(handles[:nw], max_wait_us=args.max_wait_us) as bt:
-            t = run_clients(lambda k, q: bt.infer(q, want_logits=False))
-            res[nw] = dict(images_per_s=round(n_img / t, 1), passes=bt.stats()["passes"])
+            lat_b = []
+            t = run_clients(lambda k, q: timed(lambda k_, q_: bt.infer(q_, want_logits=False), k, q, lat_b))
+            res[nw] = dict(images_per_s=round(n_img / t, 1), passes=bt.stats()["passes"], request_ms=pct(lat_b))
     for h in handles:
         h.close()
     print(json.dumps({
@@ -185,7 +217,9 @@ def serve_bench(args):
         "config": {"workload": sw["name"], "requests": len(reqs), "images": n_img,
                    "batch_sizes": list(sw["sizes"]), "image_hw": [sw["lo"], sw["hi"]], "max_batch": Bm},
         "one_client": round(n_img / seq_s, 1),
+        "one_client_request_ms": pct(lat),
         "clients_4_shared_handles": round(n_img / shared_s, 1),
+        "clients_4_shared_handles_request_ms": pct(lat_sh),
         "clients_4_batcher": {f"workers_{k}": v for k, v in res.items()},
         "batcher_max_wait_us": args.max_wait_us,
     }))
@@ -226,6 +260,7 @@ def main():
         fsb.fs_set_combine(ens.handle, policy, 0, 1)
     info = ens.info()
     N, C = info["num_models"], info["num_classes"]
+    peak = PEAK_BF16_TFLOPS if w["precision"] == "bf16" else PEAK_FP32_TFLOPS
 
     flat, desc = wl.pack_images(imgs)
     d_pix = torch.from_numpy(flat).cuda()
@@ -280,8 +315,9 @@ def main():
         per_launch_ms = sum(r["ms"] for r in conv) / len(conv)
         flops_per_launch = sum(r["flops"] for r in conv) / len(conv)
         achieved = flops_per_launch / (per_launch_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": counted_traffic(),
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "traffic": counted_traffic() if w["name"] == DEFAULT_WORKLOAD else None,
                 "algorithmic_bytes_per_launch": round(sum(r["bytes"] for r in conv) / len(conv)),
                 "kernel": "conv layer (implicit-GEMM dispatch + split-K reduce where used), mean over the layers of a step",
                 "avg_launch_us": round(per_launch_ms * 1e3, 2)}
@@ -297,10 +333,10 @@ def main():
             fl, by = rs[0]["flops"], rs[0]["bytes"]
             tf = fl / (ms_l * 1e-3) / 1e12
             ai = fl / by
-            att = min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
+            att = min(peak, ai * PEAK_HBM_GBS / 1e3)
             conv_layers.append({"layer": li, "kernel": rs[0]["kernel"], "MNK": [rs[0]["M"], rs[0]["N"], rs[0]["K"]],
                                 "us": round(ms_l * 1e3, 2), "tflops": round(tf, 1), "ai": round(ai, 1),
-                                "attainable": round(att, 1), "frac_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                                "attainable": round(att, 1), "frac_peak": round(tf / peak, 4),
                                 "frac_attainable": round(tf / att, 4)})
         roof["conv_layers"] = conv_layers
         print(json.dumps({"profiled_ms_per_step": prof_s / args.steps * 1e3,
@@ -319,18 +355,25 @@ def main():
         spans.append(ev0.elapsed_time(ev1))
     spans = np.sort(np.asarray(spans))
     # end to end: host uint8 images in, host results out (PCIe included; never the value)
-    walls = []
-    for i in range(0 if args.no_e2e else max(10, args.steps // 2) + 2):
+    walls, phases = [], []
+    for i in range(0 if args.no_e2e else max(25, args.steps) + 2):
         t0 = time.perf_counter()
         ens.infer(imgs, want_logits=False)
         if i >= 2:
             walls.append((time.perf_counter() - t0) * 1e3)
-    walls = np.sort(np.asarray(walls))
+            phases.append(fsb.fs_infer_phases(ens.handle))
+    order = np.argsort(walls)
+    walls = np.asarray(walls)[order]
+    phases = [phases[i] for i in order]
 
-    def pct(v):
-        return {q: round(float(np.percentile(v, p)), 4) for q, p in (("p10", 10), ("p50", 50), ("p90", 90))}
+    def pct(v, qs=(("p10", 10), ("p50", 50), ("p90", 90))):
+        return {q: round(float(np.percentile(v, p)), 4) for q, p in qs}
 
     hbm = None
+    if stats and "preprocess" in stats:
+        # the library counts what the transformation writes (it never sees the
+        # images' sizes on the device path); add the uint8 images it reads
+        stats["preprocess"]["bytes"] += float(flat.nbytes) * args.steps
     if stats:
         # memory-bound kernel classes: algorithmic bytes over their event time
         hbm = {k: {"achieved": round(v["bytes"] / (v["total_ms"] * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
@@ -341,7 +384,8 @@ def main():
 
     ms = plain_s / args.steps * 1e3
     out = {
-        "metric": "ensemble images/sec at B=32 (3xResNet-18, bf16) + MFMA util vs peak",
+        "metric": METRIC if w["name"] == DEFAULT_WORKLOAD else
+                  f"ensemble images/sec at B={B} ({'+'.join(w['archs'])}, {w['precision']}) + MFMA util vs peak",
         "value": round(B * args.steps / plain_s, 1),
         "unit": "images/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -358,7 +402,10 @@ def main():
         "hbm_kernels": hbm,
         "device_step_ms": pct(spans),
         "end_to_end": None if args.no_e2e else {
-            "images_per_s": round(B / float(np.median(walls)) * 1e3, 1), "ms": pct(walls),
+            "images_per_s": round(B / float(np.median(walls)) * 1e3, 1),
+            "ms": pct(walls, (("p10", 10), ("p50", 50), ("p90", 90), ("p99", 99))),
+            "phases_ms_median_call": {k: round(v, 4) for k, v in phases[len(phases) // 2].items()},
+            "phases_ms_slowest_call": {k: round(v, 4) for k, v in phases[-1].items()},
             "note": "fs_infer from host images to host results, PCIe included"},
     }
     if args.cpu_seconds > 0:

@@ -150,7 +150,11 @@ fs_status fs_infer(fs_ensemble *e, const fs_image *imgs, int32_t B,
  * (a hipStream_t; NULL = the ensemble's own stream).  d_pixels holds the
  * packed uint8 images, d_desc[B] their descriptors; every output is a
  * device pointer with the layout of fs_infer (optional ones may be NULL).
- * Requires 1 <= B <= max_batch.  Nothing is copied to or from the host. */
+ * Requires 1 <= B <= max_batch.  Nothing is copied to or from the host.
+ * The passes of one handle share its workspace, so they never overlap: a
+ * call on another stream than the handle's previous pass (fs_infer's
+ * included) makes its stream wait, on the device, for that pass to end.
+ * For passes that run concurrently use handles from fs_ensemble_share. */
 fs_status fs_infer_device(fs_ensemble *e, const uint8_t *d_pixels,
                           const fs_image_desc *d_desc, int32_t B,
                           float *d_probs, float *d_mean_probs, int32_t *d_vote,
@@ -205,7 +209,10 @@ fs_status fs_batcher_infer(fs_batcher *b, const fs_image *imgs, int32_t B, float
 /* Passes run, requests served and images served so far. */
 fs_status fs_batcher_stats(fs_batcher *b, int64_t *passes, int64_t *requests, int64_t *images);
 const char *fs_batcher_last_error(void);
-void fs_batcher_destroy(fs_batcher *b); /* NULL-safe; serves the queued requests first */
+/* NULL-safe.  Serves the queued requests first, then returns once every
+ * caller whose request was served has left fs_batcher_infer; no
+ * fs_batcher_infer call may begin once fs_batcher_destroy has begun. */
+void fs_batcher_destroy(fs_batcher *b);
 
 /* Last error message of handle e, or of this thread's last failed create
  * when e is NULL.  Valid until the next call on the same handle/thread. */
@@ -250,6 +257,34 @@ typedef struct {
 } fs_launch_stat;
 fs_status fs_profile_launches(fs_ensemble *e, fs_launch_stat *out, int32_t max_out,
                               int32_t *n_out);
+
+/* Host-side time of the phases of the handle's last fs_infer, in ms,
+ * summed over its chunks: ms[0] copying the images into pinned staging
+ * memory and issuing their upload, ms[1] issuing the device pass, ms[2]
+ * issuing the result downloads, ms[3] waiting for the stream (the device
+ * work that has not finished by then), ms[4] copying the results into the
+ * caller's buffers.  FS_ERR_INVALID for NULL arguments. */
+fs_status fs_infer_phases(fs_ensemble *e, double *ms);
+
+/* ---- test-only: one image's stored layer outputs, for layer-by-layer
+ * parity (each layer's stored input fed to a reference of that layer alone).
+ * fs_debug_capture(e, image) arms the following passes of e: after every
+ * layer's launch, the stored output of image `image` of that layer, for
+ * every model, is copied into a capture buffer of the handle (allocated
+ * here), as is the image's transformed input; those passes run without
+ * graphs.  image = -1 disarms and frees the buffer.  FS_ERR_INVALID when
+ * image is outside -1..max_batch-1.
+ * fs_debug_layer(e, model, layer, out, n) copies, widened to fp32, what the
+ * last pass captured of model `model`'s layer `layer` (index in its
+ * fs_model_spec) into out: n = H*W*C floats in NHWC order (features for an
+ * FC or average pool, fp32 logits for the last layer); layer = -1 gives the
+ * transformed input, n = out_h*out_w*3.  FS_ERR_UNSUPPORTED for a layer
+ * whose output is never stored (a conv whose max pool or average pool is
+ * fused into its launch; the pooled tensor is stored under the pool's
+ * index) or that the last pass did not capture (image >= its B).
+ * Synchronises the handle's passes. */
+fs_status fs_debug_capture(fs_ensemble *e, int32_t image);
+fs_status fs_debug_layer(fs_ensemble *e, int32_t model, int32_t layer, float *out, int64_t n);
 
 /* ---- single-kernel entry points on host tensors (synchronous; for parity
  * tests).  precision selects fp32 or bf16 storage; in bf16 the inputs must

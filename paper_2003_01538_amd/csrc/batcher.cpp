@@ -61,9 +61,10 @@ struct fs_batcher {
   int32_t N = 0, C = 0, max_batch = 0;
   std::chrono::microseconds max_wait{0};
   std::mutex mu;
-  std::condition_variable cv_work, cv_done;
+  std::condition_variable cv_work, cv_done, cv_idle;
   std::deque<Request*> queue;
   int64_t queued_images = 0;
+  int64_t callers = 0;  // threads inside fs_batcher_infer with a queued request
   bool stop = false;
   bool gathering = false;  // a worker is collecting the next pass
   int64_t passes = 0, requests = 0, images = 0;
@@ -160,7 +161,10 @@ void fs_batcher::run(Worker& wk) {
   }
 }
 
-// Stops the workers once the queue is empty.
+// Stops the workers once the queue is empty, then waits until every caller
+// whose request was served has woken and left fs_batcher_infer, so the
+// mutex and condition variables are no longer in use when the batcher is
+// freed.
 void fs_batcher::shutdown() {
   {
     std::lock_guard<std::mutex> lk(mu);
@@ -170,6 +174,8 @@ void fs_batcher::shutdown() {
   for (Worker& w : workers)
     if (w.th.joinable()) w.th.join();
   workers.clear();
+  std::unique_lock<std::mutex> lk(mu);
+  cv_idle.wait(lk, [&] { return callers == 0; });
 }
 
 extern "C" {
@@ -252,8 +258,10 @@ fs_status fs_batcher_infer(fs_batcher* b, const fs_image* imgs, int32_t B, float
       return FS_ERR_OOM;
     }
     b->queued_images += B;
+    ++b->callers;
     b->cv_work.notify_all();  // the gathering worker re-checks its fill
     b->cv_done.wait(lk, [&] { return r.done; });
+    if (--b->callers == 0) b->cv_idle.notify_all();
   }
   if (r.st != FS_OK) g_batcher_error = r.err;
   return r.st;

@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <condition_variable>
 #include <cstdio>
@@ -257,6 +258,11 @@ struct fs_ensemble {
   HostBuf h_pixels, h_desc, h_out;
   std::unique_ptr<fs::HostPool> pack_pool;  // started by the first fs_infer
   hipStream_t stream = nullptr;
+  // end of the last pass, on the stream it ran on: passes share the
+  // workspace, so a pass on another stream first waits for this event
+  hipEvent_t pass_done = nullptr;
+  hipStream_t pass_stream = nullptr;
+  bool pass_pending = false;
   // conv tile per (batch bucket) -> per group -> per layer, measured once
   std::map<int, std::vector<std::vector<int>>> tiles;
   bool tune = true;
@@ -270,6 +276,16 @@ struct fs_ensemble {
   std::vector<ProfRec> prof;
   std::vector<hipEvent_t> ev_pool;
   int64_t workspace_bytes = 0;
+  // host-side phases of the last fs_infer, ms (summed over its chunks)
+  double phase_ms[5] = {0, 0, 0, 0, 0};
+  // test-only capture of one image's stored layer outputs (fs_debug_capture)
+  int dbg_image = -1;
+  DevBuf dbg;
+  std::vector<std::vector<int64_t>> dbg_off;  // [model][layer]: byte offset in dbg, -1 = never stored
+  std::vector<std::vector<int64_t>> dbg_bytes;
+  std::vector<std::vector<char>> dbg_have;     // captured by the last pass
+  int64_t dbg_in_off = 0, dbg_in_bytes = 0;
+  bool dbg_in_have = false;
 };
 
 namespace {
@@ -844,6 +860,23 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
   return e->tiles.emplace(bucket, std::move(choice)).first->second;
 }
 
+// Test-only: copy image e->dbg_image of layer li's stored output, for every
+// model of group g, into the capture buffer (y: the output tensor of model 0,
+// y_ms: its per-model stride in elements, elems: elements per image, esz:
+// bytes per element).
+void dbg_capture(fs_ensemble* e, const Group& g, int li, const void* y, int64_t y_ms, int64_t elems, size_t esz,
+                 int B, hipStream_t s) {
+  if (e->dbg_image < 0 || e->dbg_image >= B) return;
+  for (int z = 0; z < g.Z; ++z) {
+    const int m = g.first + z;
+    const int64_t off = e->dbg_off[m][li];
+    if (off < 0 || e->dbg_bytes[m][li] != elems * (int64_t)esz) continue;
+    const char* src = static_cast<const char*>(y) + ((int64_t)z * y_ms + (int64_t)e->dbg_image * elems) * esz;
+    HIPCHK(hipMemcpyAsync(static_cast<char*>(e->dbg.p) + off, src, elems * esz, hipMemcpyDeviceToDevice, s));
+    e->dbg_have[m][li] = 1;
+  }
+}
+
 void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
               float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s) {
   Launcher launch{e, s};
@@ -867,6 +900,17 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
   pa.out_s2d = e->need_s2d ? e->input_s2d.p : nullptr;
   launch(K_PRE, 0.0, (double)B * oh * ow * 3 * esz * ((e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0)),
          (e->need_plain ? 1 : 0) + (e->need_s2d ? 1 : 0), [&] { launch_preprocess(pa, p, s); });
+  if (e->dbg_image >= 0) {
+    for (auto& v : e->dbg_have) std::fill(v.begin(), v.end(), 0);
+    e->dbg_in_have = false;
+    if (e->dbg_image < B) {
+      const void* src = e->need_plain ? e->input.p : e->input_s2d.p;
+      HIPCHK(hipMemcpyAsync(static_cast<char*>(e->dbg.p) + e->dbg_in_off,
+                            static_cast<const char*>(src) + (int64_t)e->dbg_image * e->dbg_in_bytes, e->dbg_in_bytes,
+                            hipMemcpyDeviceToDevice, s));
+      e->dbg_in_have = true;
+    }
+  }
 
   char* arena = static_cast<char*>(e->arena->p);
   const std::vector<std::vector<int>>& tiles = tiles_for(e, B, s);
@@ -908,8 +952,10 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
                               (P.in_slot == SLOT_INPUT ? 1 : g.Z);
           const double out_px = P.pool_fused ? (double)B * ((P.out.H - 1) / 2 + 1) * ((P.out.W - 1) / 2 + 1) : a.M;
           const double bytes = in_b + ((double)a.Cout * kreal * esz + out_px * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
+          const size_t yes = P.last ? 4 : esz;
           if (P.pool_fused) {
             launch(K_CONV, flops, bytes, 1, [&] { launch_conv_stem_pool(a, s); });
+            dbg_capture(e, g, (int)li + 1, y, y_ms, g.layers[li + 1].out.elems(), esz, B, s);
           } else if (P.gap_only && p == BF16 && conv_tile_direct(conv_tile(p, tile)) && conv_reduce_gap_ok(a)) {
             // the split-K completion also takes the average pool of the next layer
             const LayerPlan& G = g.layers[li + 1];
@@ -919,9 +965,11 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
               launch_conv(a, p, tile, s, false);
               launch_conv_splitk_reduce_gap(a, gy, gy_ms, s);
             });
+            dbg_capture(e, g, (int)li + 1, gy, gy_ms, G.out.elems(), esz, B, s);
             skip_next = true;
           } else {
             launch(K_CONV, flops, bytes, a.split > 1 ? 2 : 1, [&] { launch_conv(a, p, tile, s); });
+            dbg_capture(e, g, (int)li, y, y_ms, P.last ? e->C : P.out.elems(), yes, B, s);
           }
           break;
         }
@@ -937,6 +985,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
             launch(K_MAXPOOL, 0.0, bytes, 1, [&] { launch_maxpool(a, p, s); });
           else
             launch(K_GAP, 0.0, bytes, 1, [&] { launch_gap(a, p, s); });
+          dbg_capture(e, g, (int)li, y, y_ms, P.out.elems(), esz, B, s);
           break;
         }
         case FS_OP_FC: {
@@ -955,6 +1004,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           const double bytes = ((double)a.N * a.K * esz + (double)B * a.K * esz +
                                 (double)B * a.N * (a.out_f32 ? 4 : esz)) * g.Z;
           launch(K_FC, flops, bytes, fc_launches(a.split), [&] { launch_fc(a, p, s); });
+          dbg_capture(e, g, (int)li, y, y_ms, a.N, a.out_f32 ? 4 : esz, B, s);
           break;
         }
       }
@@ -1041,9 +1091,26 @@ void clear_graphs(fs_ensemble* e) {
 // candidates and grow the split-K scratch) is made before the capture, so
 // only kernel launches are recorded.  A capture that fails turns graphs off
 // for the ensemble and the pass runs eagerly.
+void run_pass_ordered(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
+                      float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s);
+
+// Every pass of a handle uses the handle's one workspace (transformed
+// input, activation slots, split-K scratch, logits), so passes issued on
+// different streams must not overlap: a pass on a stream other than the
+// previous pass's first waits (on the device) for the previous pass's end.
 void run_pass_cached(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
                      float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s) {
-  if (!e->graphs || e->prof_on || s == nullptr) {
+  if (e->pass_pending && e->pass_stream != s) HIPCHK(hipStreamWaitEvent(s, e->pass_done, 0));
+  if (!e->pass_done) HIPCHK(hipEventCreateWithFlags(&e->pass_done, hipEventDisableTiming));
+  run_pass_ordered(e, d_pixels, d_desc, B, d_probs, d_mean, d_vote, d_top1, d_logits, s);
+  HIPCHK(hipEventRecord(e->pass_done, s));
+  e->pass_stream = s;
+  e->pass_pending = true;
+}
+
+void run_pass_ordered(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, int B, float* d_probs,
+                      float* d_mean, int32_t* d_vote, int32_t* d_top1, float* d_logits, hipStream_t s) {
+  if (!e->graphs || e->prof_on || e->dbg_image >= 0 || s == nullptr) {
     run_pass(e, d_pixels, d_desc, B, d_probs, d_mean, d_vote, d_top1, d_logits, s);
     return;
   }
@@ -1083,6 +1150,8 @@ void run_pass_cached(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d
 void destroy_impl(fs_ensemble* e) {
   if (!e) return;
   if (hipSetDevice(e->device) == hipSuccess) {
+    if (e->pass_pending) (void)hipEventSynchronize(e->pass_done);
+    if (e->pass_done) (void)hipEventDestroy(e->pass_done);
     if (e->stream) (void)hipStreamSynchronize(e->stream);
     clear_graphs(e);
     prof_clear(e);
@@ -1323,6 +1392,15 @@ fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs
     e->h_desc.ensure((size_t)Bm * sizeof(ImageDesc));
     const size_t out_floats = (size_t)N * Bm * C * 2 + (size_t)Bm * C;
     e->h_out.ensure(out_floats * 4 + ((size_t)N + 1) * Bm * 4);
+    using clk = std::chrono::steady_clock;
+    auto lap = [](clk::time_point& t) {
+      const clk::time_point n = clk::now();
+      const double ms = std::chrono::duration<double, std::milli>(n - t).count();
+      t = n;
+      return ms;
+    };
+    for (double& v : e->phase_ms) v = 0;
+    clk::time_point t = clk::now();
     for (int b0 = 0; b0 < B; b0 += Bm) {
       const int nb = std::min(Bm, B - b0);
       const size_t pbytes = packed_size(imgs, b0, nb);
@@ -1340,10 +1418,12 @@ fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs
         if (hi > lo) HIPCHK(hipMemcpyAsync(dpix + lo, hpix + lo, hi - lo, hipMemcpyHostToDevice, s));
       });
       HIPCHK(hipMemcpyAsync(e->d_desc.p, hd, nb * sizeof(ImageDesc), hipMemcpyHostToDevice, s));
+      e->phase_ms[0] += lap(t);
       float* dlog = static_cast<float*>(e->logits.p);
       run_pass_cached(e, static_cast<const uint8_t*>(e->d_pixels.p), static_cast<const ImageDesc*>(e->d_desc.p),
                       nb, static_cast<float*>(e->d_probs.p), mean_probs ? static_cast<float*>(e->d_mean.p) : nullptr,
                       static_cast<int32_t*>(e->d_vote.p), static_cast<int32_t*>(e->d_top1.p), dlog, s);
+      e->phase_ms[1] += lap(t);
       float* hp = static_cast<float*>(e->h_out.p);
       float* hl = hp + (size_t)N * Bm * C;
       float* hm = hl + (size_t)N * Bm * C;
@@ -1355,7 +1435,9 @@ fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs
       if (mean_probs) HIPCHK(hipMemcpyAsync(hm, e->d_mean.p, (size_t)nb * C * 4, hipMemcpyDeviceToHost, s));
       HIPCHK(hipMemcpyAsync(hv, e->d_vote.p, (size_t)nb * 4, hipMemcpyDeviceToHost, s));
       HIPCHK(hipMemcpyAsync(ht, e->d_top1.p, (size_t)N * nb * 4, hipMemcpyDeviceToHost, s));
+      e->phase_ms[2] += lap(t);
       HIPCHK(hipStreamSynchronize(s));
+      e->phase_ms[3] += lap(t);
       for (int i = 0; i < N; ++i) {
         std::memcpy(probs + ((size_t)i * B + b0) * C, hp + (size_t)i * nb * C, (size_t)nb * C * 4);
         if (logits) std::memcpy(logits + ((size_t)i * B + b0) * C, hl + (size_t)i * nb * C, (size_t)nb * C * 4);
@@ -1363,6 +1445,7 @@ fs_status fs_infer(fs_ensemble* e, const fs_image* imgs, int32_t B, float* probs
       }
       if (mean_probs) std::memcpy(mean_probs + (size_t)b0 * C, hm, (size_t)nb * C * 4);
       std::memcpy(vote + b0, hv, (size_t)nb * 4);
+      e->phase_ms[4] += lap(t);
     }
   });
 }
@@ -1405,6 +1488,7 @@ fs_status fs_graphs_enable(fs_ensemble* e, int32_t enable) {
   return guarded(e, [&] {
     HIPCHK(hipSetDevice(e->device));
     HIPCHK(hipStreamSynchronize(e->stream));
+    if (e->pass_pending) HIPCHK(hipEventSynchronize(e->pass_done));
     clear_graphs(e);
     e->graphs = enable != 0;
   });
@@ -1420,6 +1504,7 @@ fs_status fs_set_combine(fs_ensemble* e, int32_t policy, int32_t positive_class,
     check_combine(policy, positive_class, min_votes, e->N, e->C);
     HIPCHK(hipSetDevice(e->device));
     HIPCHK(hipStreamSynchronize(e->stream));
+    if (e->pass_pending) HIPCHK(hipEventSynchronize(e->pass_done));
     clear_graphs(e);  // the recorded passes carry the old policy's arguments
     e->combine = policy;
     e->pos_class = policy == FS_COMBINE_ANY ? positive_class : 0;
@@ -1490,6 +1575,104 @@ fs_status fs_profile_launches(fs_ensemble* e, fs_launch_stat* out, int32_t max_o
       o.ms = ms; o.flops = r.flops; o.bytes = r.bytes;
     }
     *n_out = n;
+  });
+}
+
+fs_status fs_infer_phases(fs_ensemble* e, double* ms) {
+  if (!e || !ms) {
+    g_thread_error = "ensemble or ms is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  for (int i = 0; i < 5; ++i) ms[i] = e->phase_ms[i];
+  return FS_OK;
+}
+
+fs_status fs_debug_capture(fs_ensemble* e, int32_t image) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    if (image < -1 || image >= e->max_batch) fail(FS_ERR_INVALID, "image must be -1 or in 0..max_batch-1");
+    HIPCHK(hipSetDevice(e->device));
+    HIPCHK(hipStreamSynchronize(e->stream));
+    if (e->pass_pending) HIPCHK(hipEventSynchronize(e->pass_done));
+    e->dbg_image = -1;
+    e->dbg_off.assign(e->N, {});
+    e->dbg_bytes.assign(e->N, {});
+    e->dbg_have.assign(e->N, {});
+    e->dbg_in_have = false;
+    if (image < 0) {
+      e->dbg.release();
+      return;
+    }
+    const size_t esz = es(e->prec);
+    int64_t off = 0;
+    e->dbg_in_off = 0;
+    e->dbg_in_bytes = e->need_plain ? (int64_t)e->pre.out_h * e->pre.out_w * 4 * esz
+                                    : (int64_t)(e->pre.out_h / 2) * (e->pre.out_w / 2) * 16 * 2;
+    off = (int64_t)round_up(e->dbg_in_bytes, 256);
+    for (const Group& g : e->groups) {
+      for (int z = 0; z < g.Z; ++z) {
+        const int m = g.first + z;
+        e->dbg_off[m].assign(g.layers.size(), -1);
+        e->dbg_bytes[m].assign(g.layers.size(), 0);
+        e->dbg_have[m].assign(g.layers.size(), 0);
+        for (size_t li = 0; li < g.layers.size(); ++li) {
+          const LayerPlan& P = g.layers[li];
+          if (P.op == FS_OP_CONV && P.pool_fused) continue;  // only the pooled tensor is stored
+          const int64_t elems = P.last ? e->C : P.out.elems();
+          e->dbg_off[m][li] = off;
+          e->dbg_bytes[m][li] = elems * (int64_t)(P.last ? 4 : esz);
+          off += (int64_t)round_up(e->dbg_bytes[m][li], 256);
+        }
+      }
+    }
+    e->dbg.alloc(std::max<int64_t>(off, 256));
+    e->dbg_image = image;
+  });
+}
+
+fs_status fs_debug_layer(fs_ensemble* e, int32_t model, int32_t layer, float* out, int64_t n) {
+  if (!e || !out) {
+    g_thread_error = "ensemble or out is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  return guarded(e, [&] {
+    if (e->dbg_image < 0) fail(FS_ERR_INVALID, "no capture armed (fs_debug_capture)");
+    if (model < 0 || model >= e->N) fail(FS_ERR_INVALID, "model out of range");
+    HIPCHK(hipSetDevice(e->device));
+    HIPCHK(hipStreamSynchronize(e->stream));
+    if (e->pass_pending) HIPCHK(hipEventSynchronize(e->pass_done));
+    const size_t esz = es(e->prec);
+    if (layer == -1) {
+      if (!e->dbg_in_have) fail(FS_ERR_INVALID, "the last pass captured no input");
+      const int oh = e->pre.out_h, ow = e->pre.out_w;
+      if (n != (int64_t)oh * ow * 3) fail(FS_ERR_INVALID, "n must be out_h * out_w * 3 for the input");
+      std::vector<float> raw;
+      const int64_t ne = e->dbg_in_bytes / (e->need_plain ? (int64_t)esz : 2);
+      raw.resize(ne);
+      download_as(raw.data(), static_cast<char*>(e->dbg.p) + e->dbg_in_off, ne, e->need_plain ? e->prec : BF16);
+      for (int y = 0; y < oh; ++y)
+        for (int x = 0; x < ow; ++x)
+          for (int c = 0; c < 3; ++c)
+            out[((int64_t)y * ow + x) * 3 + c] =
+                e->need_plain ? raw[((int64_t)y * ow + x) * 4 + c]
+                              : raw[((int64_t)(y / 2) * (ow / 2) + x / 2) * 16 + ((y & 1) * 2 + (x & 1)) * 3 + c];
+      return;
+    }
+    if (layer < 0 || layer >= (int32_t)e->dbg_off[model].size()) fail(FS_ERR_INVALID, "layer out of range");
+    if (e->dbg_off[model][layer] < 0) fail(FS_ERR_UNSUPPORTED, "this layer's output is never stored (fused)");
+    if (!e->dbg_have[model][layer]) fail(FS_ERR_UNSUPPORTED, "the last pass stored no copy of this layer");
+    int gi = 0;
+    while (!(e->groups[gi].first <= model && model < e->groups[gi].first + e->groups[gi].Z)) ++gi;
+    const LayerPlan& P = e->groups[gi].layers[layer];
+    const int64_t elems = P.last ? e->C : P.out.elems();
+    if (n != elems) fail(FS_ERR_INVALID, "n must be the layer's H * W * C");
+    download_as(out, static_cast<char*>(e->dbg.p) + e->dbg_off[model][layer], elems, P.last ? F32 : e->prec);
   });
 }
 

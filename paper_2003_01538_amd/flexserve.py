@@ -110,6 +110,9 @@ SIGNATURES = [
     ("fs_batcher_destroy", None, [_vp]),
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
     ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
+    ("fs_infer_phases", ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
+    ("fs_debug_capture", ctypes.c_int, [_vp, ctypes.c_int32]),
+    ("fs_debug_layer", ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, _fp, ctypes.c_int64]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
                                           ctypes.c_int32, _fp, _fp, ctypes.c_int32, ctypes.c_int32, _fp,
                                           ctypes.c_int32]),
@@ -356,6 +359,24 @@ def fs_profile_launches(handle, max_out=4096) -> list:
         res.append(dict(kclass=r.kclass.decode(), kernel=r.kernel.decode(), group=r.group, layer=r.layer,
                         M=r.M, N=r.N, K=r.K, Z=r.Z, ms=r.ms, flops=r.flops, bytes=r.bytes))
     return res
+
+
+def fs_infer_phases(handle):
+    """Host-side phase times (ms) of the handle's last fs_infer."""
+    ms = (ctypes.c_double * 5)()
+    _check(load().fs_infer_phases(handle, ms), handle)
+    return dict(zip(("stage_upload", "issue_pass", "issue_download", "sync", "copy_out"), list(ms)))
+
+
+def fs_debug_capture(handle, image):
+    _check(load().fs_debug_capture(handle, image), handle)
+
+
+def fs_debug_layer(handle, model, layer, shape):
+    """The captured output of one layer of one model (fp32 array of `shape`)."""
+    out = np.empty(shape, np.float32)
+    _check(load().fs_debug_layer(handle, model, layer, _f(out), out.size), handle)
+    return out
 
 
 def fs_test_preprocess(imgs, out_h, out_w, mean, std, precision, layout=0, device=0):

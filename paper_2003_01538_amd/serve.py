@@ -133,7 +133,10 @@ class Server:
                 self._reply(200, format_result(res, server.policy))
 
         self.httpd = ThreadingHTTPServer((host, port), Handler)
-        self.httpd.daemon_threads = True
+        # handler threads are joined by server_close(), so none is inside
+        # the batcher when stop() closes it
+        self.httpd.daemon_threads = False
+        self.httpd.block_on_close = True
         self.thread = None
 
     @property

@@ -2,22 +2,27 @@
 ensemble outputs (test infrastructure).
 
 fp32 storage:   max |p_gpu - p_orc| <= 1e-4; top-1 identical where the
-                oracle's top-2 logit margin exceeds 1e-2; vote identical where
-                the top-2 margin of S = sum_i p_i exceeds 2*N*1e-4.
+                oracle's top-2 logit margin exceeds max(1e-2, 4*nu); vote
+                identical where the top-2 margin of S = sum_i p_i exceeds
+                2*N*1e-4.
 bf16 storage:   compared with the oracle in bf16-storage mode.
                 max |p_gpu - p_orc| <= 2e-2; scale-free logit gate
                 max |z_gpu - z_orc| / std(z_orc[row]) <= 3e-2; top-1
-                identical where the margin exceeds max(1e-2, 6e-2*std) (two
-                logits can each move by 3e-2*std); top-1 agreement >= 99.5%;
-                vote identical where the S margin exceeds 2*N*2e-2, else the
-                GPU vote lies within 2*N*2e-2 of the oracle's maximum of S.
+                identical where the margin exceeds max(1e-2, 4*nu); top-1
+                agreement >= 99.5%; vote identical where the S margin exceeds
+                2*N*2e-2, else the GPU vote lies within 2*N*2e-2 of the
+                oracle's maximum of S.
 
-The oracle's own noise floor: when the oracle is rerun with fp32 sequential
-accumulation (o32), the difference nu from its double-accumulation run is
-what a change of summation order alone does to that row (bf16 storage makes
-random ResNets chaotic: one flipped bf16 rounding early moves late logits).
-A row whose nu exceeds the gate cannot be resolved by it; its gates widen to
-2*nu (probabilities, logits) and its top-1 exemption margin to 4*nu.
+nu is the oracle's own noise floor for a row: the oracle rerun with fp32
+sequential accumulation (o32) differs from its double-accumulation run only
+in summation order, and max |z_o32 - z_orc| over the row is what a change of
+order alone does to its logits (bf16 storage makes random deep networks
+chaotic: one flipped bf16 rounding early moves late logits).  A row whose
+probability noise exceeds half the probability gate cannot be resolved by
+that gate: its probability and logit gates become 2*nu and the row is listed
+in the report (`widened`), with the GPU's deviation, so the literal result
+is always visible.  The layer-by-layer parity tests (every layer fed the
+GPU's own stored input) are the check that is not chaotic.
 """
 import numpy as np
 
@@ -46,6 +51,13 @@ def oracle_acc32(models, imgs, out_hw, mean, std, prec, prepared=None):
         oracle.set_acc32(False)
 
 
+def _nu(o, o32, i, b):
+    if o32 is None:
+        return 0.0, 0.0
+    return (float(np.abs(o32["probs"][i, b] - o["probs"][i, b]).max()),
+            float(np.abs(o32["logits"][i, b] - o["logits"][i, b]).max()))
+
+
 def compare(g, o, prec, idx=None, report=None, o32=None):
     """g: GPU outputs over the whole batch; o: oracle outputs for images idx
     (all when None).  Raises AssertionError with a description."""
@@ -56,31 +68,31 @@ def compare(g, o, prec, idx=None, report=None, o32=None):
     gv, gt = g["vote"][sel], g["top1"][:, sel]
     op, oz, ov, ot, oS = o["probs"], o["logits"], o["vote"], o["top1"], o["S"]
     dp = np.abs(gp - op).max()
-    agree, total, exempt, widened = 0, 0, 0, 0
+    agree, total, exempt, over_literal = 0, 0, 0, 0
+    widened = []
     worst_rel = 0.0
     nu_p_max = 0.0
     gate_img = np.full(op.shape[1], t["p"])
     for i in range(N):
         for b in range(op.shape[1]):
             sd = float(np.std(oz[i, b]))
-            nu_p = nu_z = 0.0
-            if o32 is not None:
-                nu_p = float(np.abs(o32["probs"][i, b] - op[i, b]).max())
-                nu_z = float(np.abs(o32["logits"][i, b] - oz[i, b]).max())
-                nu_p_max = max(nu_p_max, nu_p)
+            nu_p, nu_z = _nu(o, o32, i, b)
+            nu_p_max = max(nu_p_max, nu_p)
             dpr = float(np.abs(gp[i, b] - op[i, b]).max())
-            gate_p = max(t["p"], 2 * nu_p)
-            widened += int(gate_p > t["p"])
+            over_literal += int(dpr > t["p"])
+            gate_p, gate_z = t["p"], t["logit_rel"]
+            if nu_p > t["p"] / 2:  # the oracle cannot resolve the literal gate on this row
+                gate_p = max(t["p"], 2 * nu_p)
+                if gate_z is not None:
+                    gate_z = max(gate_z, 2 * nu_z / max(sd, 1e-30))
+                widened.append(dict(model=i, image=int(b if idx is None else idx[b]), dp=dpr, nu_p=nu_p))
             gate_img[b] = max(gate_img[b], gate_p)
             assert dpr <= gate_p, f"model {i} image {b}: max |dp| = {dpr:.3g} > {gate_p:.3g} (nu {nu_p:.3g})"
-            if t["logit_rel"] is not None:
+            if gate_z is not None:
                 rel = float(np.abs(gz[i, b] - oz[i, b]).max() / max(sd, 1e-30))
                 worst_rel = max(worst_rel, rel)
-                gate_z = max(t["logit_rel"], 2 * nu_z / max(sd, 1e-30))
                 assert rel <= gate_z, f"model {i} image {b}: logit error {rel:.3g} of std > {gate_z:.3g}"
-                thr = max(t["margin"], 2 * t["logit_rel"] * sd, 4 * nu_z)
-            else:
-                thr = max(t["margin"], 4 * nu_z)
+            thr = max(t["margin"], 4 * nu_z)
             total += 1
             agree += int(gt[i, b] == ot[i, b])
             if _top2_margin(oz[i, b]) > thr:
@@ -96,5 +108,35 @@ def compare(g, o, prec, idx=None, report=None, o32=None):
         else:
             assert oS[b, gv[b]] >= oS[b].max() - vt, f"image {b}: vote {gv[b]} not near the maximum"
     if report is not None:
-        report.update(max_dp=float(dp), top1_agree=agree / total, exempt=exempt,
-                      worst_logit_rel=worst_rel, oracle_nu_p=nu_p_max, rows_widened=widened)
+        report.update(max_dp=float(dp), rows=total, rows_over_literal=over_literal, top1_agree=agree / total,
+                      exempt=exempt, worst_logit_rel=worst_rel, oracle_nu_p=nu_p_max,
+                      rows_widened=len(widened), widened=widened)
+
+
+def compare_classes(top1, vote, o, prec, o32=None, idx=None):
+    """Class ids only (what the HTTP front end returns): top1 [N][B'] and
+    vote [B'] of the GPU for images idx against the oracle's, with the
+    margin rules of compare()."""
+    t = TOL[prec]
+    N = o["top1"].shape[0]
+    sel = slice(None) if idx is None else np.asarray(idx)
+    gt, gv = np.asarray(top1)[:, sel], np.asarray(vote)[sel]
+    checked = 0
+    for i in range(N):
+        for b in range(o["top1"].shape[1]):
+            nu_p, nu_z = _nu(o, o32, i, b)
+            if _top2_margin(o["logits"][i, b]) > max(t["margin"], 4 * nu_z):
+                assert gt[i, b] == o["top1"][i, b], f"model {i} image {b}: top1 {gt[i, b]} vs {o['top1'][i, b]}"
+                checked += 1
+    for b in range(o["S"].shape[0]):
+        gate = t["p"]
+        for i in range(N):
+            nu_p, _ = _nu(o, o32, i, b)
+            if nu_p > t["p"] / 2:
+                gate = max(gate, 2 * nu_p)
+        vt = 2 * N * gate
+        if _top2_margin(o["S"][b]) > vt:
+            assert gv[b] == o["vote"][b], f"image {b}: vote {gv[b]} vs {o['vote'][b]}"
+        else:
+            assert o["S"][b, gv[b]] >= o["S"][b].max() - vt, f"image {b}: vote {gv[b]} not near the maximum"
+    return checked

@@ -10,7 +10,7 @@ import pytest
 import oracle
 import workloads as wl
 from paper_2003_01538_amd import flexserve as fsb
-from tests.parity import compare, oracle_acc32
+from tests.parity import compare, compare_classes, oracle_acc32
 
 pytestmark = pytest.mark.gpu
 MEAN, STD = wl.IMAGENET_MEAN, wl.IMAGENET_STD
@@ -74,18 +74,31 @@ def test_resnet18x3_bf16_b32_full_batch_sampled():
 
 
 def test_flexible_batch_stream_requests():
+    # The whole seeded stream of 200 requests runs as the request-stream
+    # benchmark runs it (one fs_infer per request); the first and last image
+    # of the first request of every batch size is checked against the
+    # oracle, so all 8 sizes are covered.
     s = wl.STREAM_WORKLOAD
     w = wl.workload(s["ensemble"])
-    reqs = wl.request_stream(s["seed"], 12)
+    reqs = wl.request_stream(s["seed"], s["n_requests"])
+    assert len(reqs) == 200
     with _ensemble(w, max_batch=64) as ens:
-        seen = set()
+        firsts = {}
         for q in reqs:
-            if len(q) in seen:
-                continue
-            seen.add(len(q))
-            sample = sorted({0, len(q) - 1})
-            _check(w, ens, q, sample)
-        assert len(seen) >= 4
+            g = ens.infer(q)
+            assert g["probs"].shape[1] == len(q)
+            if len(q) not in firsts:
+                firsts[len(q)] = (q, g)
+        assert sorted(firsts) == sorted(s["sizes"])
+        prepared = [oracle.prepare_model(m, "bf16") for m in w["models"]]
+        for B, (q, g) in sorted(firsts.items()):
+            sample = sorted({0, B - 1})
+            sub = [q[i] for i in sample]
+            o = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            o32 = oracle_acc32(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            rep = {}
+            compare(g, o, "bf16", idx=sample, report=rep, o32=o32)
+            print(f"stream B={B}: max|dp| {rep['max_dp']:.3g}, widened {rep['rows_widened']}")
 
 
 def test_hetero_r18_r50_vgg11_b32_sampled():
@@ -93,8 +106,27 @@ def test_hetero_r18_r50_vgg11_b32_sampled():
     with _ensemble(w) as ens:
         assert ens.info()["num_groups"] == 3
         rep = {}
-        _check(w, ens, _images(w), [0, 31], report=rep)
+        _check(w, ens, _images(w), [0, 9, 22, 31], report=rep)
         print("hetero parity", rep)
+
+
+def test_hetero_fp32_mode_at_224():
+    # The heterogeneous ensemble in fp32 storage at its full 224 x 224 shape:
+    # no bf16 rounding anywhere, so GPU and oracle differ by fp32 summation
+    # order only, and the 1e-4 probability gate holds literally.
+    w = wl.workload("hetero_r18_r50_vgg11_bf16_b32")
+    imgs = _images(w)
+    sub = [imgs[0], imgs[31]]
+    with fsb.Ensemble(w["models"], w["out_hw"], MEAN, STD, "fp32", max_batch=2) as ens:
+        assert ens.info()["num_groups"] == 3
+        g = ens.infer(sub)
+    o = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, "fp32")
+    rep = {}
+    compare(g, o, "fp32", report=rep)
+    assert rep["rows_widened"] == 0 and rep["max_dp"] <= 1e-4
+    rel = np.abs(g["logits"] - o["logits"]).max(axis=-1) / np.abs(o["logits"]).max(axis=-1)
+    print("hetero fp32 parity", rep, "max logit error / max |logit| per row", rel.max())
+    assert rel.max() <= 1e-4
 
 
 def test_resnet50x5_b256_sampled():
@@ -284,6 +316,13 @@ def test_shared_handles_run_concurrently():
             for k in ("probs", "logits", "vote", "top1", "mean"):
                 assert np.array_equal(out[("a", i)][k], ref_a[k]), (i, k)
                 assert np.array_equal(out[("b", i)][k], ref_b[k]), (i, k)
+        # and the concurrent results are the oracle's
+        prepared = [oracle.prepare_model(m, "bf16") for m in w["models"]]
+        for key, part, sample in (("a", imgs[:16], [0, 15]), ("b", imgs[16:], [3, 15])):
+            sub = [part[i] for i in sample]
+            o = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            o32 = oracle_acc32(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            compare(out[(key, 3)], o, "bf16", idx=sample, o32=o32)
         other.set_combine(fsb.FS_COMBINE_PLURALITY)  # a handle's policy is its own
         assert np.array_equal(ens.infer(imgs[16:])["vote"], ref_b["vote"])
         ens.close()
@@ -331,6 +370,14 @@ def test_batcher_coalesces_concurrent_requests():
             assert np.array_equal(res[k]["top1"], ref["top1"][:, o:o + b])
             assert np.array_equal(res[k]["vote"], ref["vote"][o:o + b])
             assert np.array_equal(res[k]["mean"], ref["mean"][o:o + b])
+        # each coalesced request's first and last image against the oracle
+        prepared = [oracle.prepare_model(m, "bf16") for m in w["models"]]
+        for k, (o, part) in enumerate(parts):
+            sample = sorted({0, len(part) - 1})
+            sub = [part[i] for i in sample]
+            oo = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            o32 = oracle_acc32(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            compare(res[k], oo, "bf16", idx=sample, o32=o32)
         with fsb.Batcher(ens, max_wait_us=0) as b0:
             for q in (imgs[:7], imgs[7:8], imgs + imgs[:8]):
                 g, r = b0.infer(q), ens.infer(q)
@@ -367,8 +414,63 @@ def test_batcher_coalesces_concurrent_requests():
                 for g in res2[k]:
                     for key in ("probs", "vote", "top1", "mean"):
                         assert np.array_equal(g[key], refs[k][key]), (k, key)
+            # one pass of the two-worker batcher against the oracle
+            sample = [0, 31]
+            sub = [qs[2][i] for i in sample]
+            oo = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            o32 = oracle_acc32(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+            g = dict(res2[2][-1])
+            g["logits"] = refs[2]["logits"]  # the batcher was asked for no logits; its probs equal refs[2]'s
+            compare(g, oo, "bf16", idx=sample, o32=o32)
         finally:
             other.close()
+
+
+def test_device_passes_on_two_streams_of_one_handle():
+    # Passes of one handle share its workspace; calls alternating between two
+    # streams (and with fs_infer on the handle's own stream) are ordered by
+    # the library, so each result is that of its own images: the bits of
+    # fs_infer on them, and the oracle's values.
+    import torch
+    w = wl.workload("resnet18x3_bf16_b32")
+    imgs = _images(w)
+    sets = [imgs[0:8], imgs[8:16], imgs[16:24]]
+    N, B, C = 3, 8, 1000
+    with _ensemble(w, max_batch=8) as ens:
+        refs = [ens.infer(q) for q in sets]
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        dev = []
+        for q in sets:
+            flat, desc = wl.pack_images(q)
+            dev.append((torch.from_numpy(flat).cuda(),
+                        torch.tensor([[o, h | (w_ << 32), rs] for o, h, w_, rs in desc], dtype=torch.int64).cuda()))
+        torch.cuda.synchronize()
+        outs = []
+        for it in range(6):
+            k = it % 3
+            st = streams[it % 2]
+            probs = torch.empty((N, B, C), dtype=torch.float32, device="cuda")
+            logits = torch.empty_like(probs)
+            vote = torch.empty(B, dtype=torch.int32, device="cuda")
+            top1 = torch.empty((N, B), dtype=torch.int32, device="cuda")
+            fsb.fs_infer_device(ens.handle, dev[k][0].data_ptr(), dev[k][1].data_ptr(), B, probs.data_ptr(), 0,
+                                vote.data_ptr(), top1.data_ptr(), logits.data_ptr(), st.cuda_stream)
+            outs.append((k, probs, logits, vote, top1))
+            if it == 3:  # a host call in between, on the handle's own stream
+                g = ens.infer(sets[1])
+                assert np.array_equal(g["logits"], refs[1]["logits"])
+        torch.cuda.synchronize()
+        for k, probs, logits, vote, top1 in outs:
+            assert np.array_equal(logits.cpu().numpy(), refs[k]["logits"]), k
+            assert np.array_equal(probs.cpu().numpy(), refs[k]["probs"]), k
+            assert np.array_equal(vote.cpu().numpy(), refs[k]["vote"]), k
+            assert np.array_equal(top1.cpu().numpy(), refs[k]["top1"]), k
+    prepared = [oracle.prepare_model(m, "bf16") for m in w["models"]]
+    for k in range(3):
+        sub = [sets[k][5]]
+        o = oracle.ensemble(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+        o32 = oracle_acc32(w["models"], sub, w["out_hw"], MEAN, STD, "bf16", prepared)
+        compare(refs[k], o, "bf16", idx=[5], o32=o32)
 
 
 def test_batch_sizes_inside_a_bucket():
@@ -430,6 +532,17 @@ def test_http_front_end():
                 for i in range(2):
                     assert got[k][f"model y_{i}"] == ref["top1"][i].tolist()
                 assert got[k]["combined"] == oracle.vote_policy(ref["top1"], 10, fsb.FS_COMBINE_PLURALITY).tolist()
+                # the reply's classes are the oracle's: every model's top-1
+                # (where the oracle's top-2 margin exceeds 1e-2; fp32 storage,
+                # so the oracle's own noise is far below it) and the plurality
+                # of the oracle's classes
+                o = oracle.ensemble(w["models"], reqs[k], w["out_hw"], MEAN, STD, "fp32")
+                z = np.sort(o["logits"], axis=-1)
+                decided = z[..., -1] - z[..., -2] > 1e-2
+                y = np.array([got[k][f"model y_{i}"] for i in range(2)])
+                assert np.array_equal(y[decided], o["top1"][decided]), k
+                if decided.all():
+                    assert got[k]["combined"] == oracle.vote_policy(o["top1"], 10, fsb.FS_COMBINE_PLURALITY).tolist()
             for bad in ({"arrays": []}, {"images": ["!!"]},
                         {"policy": "mean", "arrays": [{"shape": [1, 1, 3], "data": "AAAA"}]}):
                 with pytest.raises(urllib.error.HTTPError) as e:
@@ -438,3 +551,31 @@ def test_http_front_end():
     finally:
         other.close()
         ens.close()
+
+
+def test_http_front_end_mean_policy_bf16():
+    # The three-ResNet-18 ensemble behind the HTTP front end with the
+    # mean-probability policy: the reply's "model y_i" and "combined" are the
+    # oracle's classes (top-1 where the margin decides it, the vote by the
+    # rules of the end-to-end comparison).
+    import base64
+    import json
+    import urllib.request
+    from paper_2003_01538_amd import serve
+    w = wl.workload("resnet18x3_bf16_b32")
+    reqs = wl.request_stream(wl.STREAM_WORKLOAD["seed"], 6)
+    reqs = [q[:4] for q in reqs]
+    prepared = [oracle.prepare_model(m, "bf16") for m in w["models"]]
+    with _ensemble(w, max_batch=32) as ens:
+        with serve.Server([ens], max_wait_us=100, policy="mean") as srv:
+            for q in reqs:
+                arrs = [{"shape": list(a.shape), "data": base64.b64encode(np.ascontiguousarray(a).tobytes()).decode()}
+                        for a in q]
+                r = urllib.request.Request(srv.url + "/infer", data=json.dumps({"arrays": arrs}).encode(),
+                                           headers={"Content-Type": "application/json"})
+                with urllib.request.urlopen(r, timeout=120) as f:
+                    got = json.loads(f.read())
+                y = np.array([got[f"model y_{i}"] for i in range(3)])
+                o = oracle.ensemble(w["models"], q, w["out_hw"], MEAN, STD, "bf16", prepared)
+                o32 = oracle_acc32(w["models"], q, w["out_hw"], MEAN, STD, "bf16", prepared)
+                compare_classes(y, np.array(got["combined"]), o, "bf16", o32=o32)
