@@ -352,6 +352,31 @@ fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Co
                         int32_t precision, int32_t tile, int32_t Z, int32_t iters, double *avg_ms,
                         int32_t *tile_used, int32_t device);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): one bf16
+ * convolution on device-resident tensors, computed by the kernels and the
+ * tile and split-K rule fs_test_conv uses with tile = -1 (same bits).  It
+ * calls no allocating routine: the split-K partial sums go to a
+ * library-static device array of FS_NOALLOC_SCRATCH_BYTES per GPU (each GPU
+ * the library runs on holds it until the process ends).  Every call on one
+ * GPU shares that array, so calls that overlap on one GPU (concurrent
+ * streams, several threads) race; calls issued on one stream are ordered.
+ * Runs on the current device, asynchronously on `stream` (a hipStream_t,
+ * NULL = the null stream).
+ *   d_in   [B][H][W][Cin] bf16, Cin a multiple of 64
+ *   d_w    [Cout][kh][kw][Cin] bf16, Cout a multiple of 8
+ *   d_bias [Cout] fp32, required
+ *   d_res  [B][Ho][Wo][Cout] bf16 added before the ReLU, or NULL
+ *   d_out  [B][Ho][Wo][Cout] bf16 = bf16(relu?(conv + bias + res))
+ * FS_ERR_INVALID for NULL or inconsistent arguments; FS_ERR_UNSUPPORTED
+ * for channel counts outside the above, tensors of 2 GiB or more, or a
+ * shape whose partial sums exceed the scratch array. */
+#define FS_NOALLOC_SCRATCH_BYTES (16 << 20)
+fs_status fs_conv_bf16_device_noalloc(const void *d_in, int32_t B, int32_t H, int32_t W, int32_t Cin,
+                                      const void *d_w, const float *d_bias, const void *d_res,
+                                      int32_t Cout, int32_t kh, int32_t kw, int32_t stride,
+                                      int32_t pad, int32_t relu, void *d_out, void *stream);
+
 /* Number of conv tile configurations fs_test_conv accepts (0..n-1) for a
  * precision, and the name of tile t (NULL when out of range). */
 int32_t fs_conv_num_tiles(int32_t precision);

@@ -1283,10 +1283,74 @@ void pack_images_staged(const fs_image* imgs, int b0, int nb, uint8_t* dst, Imag
   }
 }
 
+// ------------------------------------------- allocation-free convolution
+// The split-K partial sums of fs_conv_bf16_device_noalloc live in this
+// library-static device array: every GPU the library runs on holds its own
+// copy until the process ends.  In host code the name is only a stand-in;
+// its device address comes from hipGetSymbolAddress, once per device, and
+// only that address is passed to kernels.
+constexpr size_t kNoallocScratchFloats = (size_t)FS_NOALLOC_SCRATCH_BYTES / 4;
+static __device__ __align__(256) float scratch[kNoallocScratchFloats];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch` (looked up on its first use there).
+float* noalloc_scratch(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) fail(FS_ERR_DEVICE, "device ordinal outside 0..63");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) fail(FS_ERR_DEVICE, "no device address for the scratch array");
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 // ==================================================================== ABI
 extern "C" {
+
+fs_status fs_conv_bf16_device_noalloc(const void* d_in, int32_t B, int32_t H, int32_t W, int32_t Cin, const void* d_w,
+                                      const float* d_bias, const void* d_res, int32_t Cout, int32_t kh, int32_t kw,
+                                      int32_t stride, int32_t pad, int32_t relu, void* d_out, void* stream) {
+  return guarded(nullptr, [&] {
+    if (!d_in || !d_w || !d_bias || !d_out) fail(FS_ERR_INVALID, "input, weight, bias and output are required");
+    if (B < 1 || H < 1 || W < 1 || Cin < 1 || Cout < 1 || kh < 1 || kw < 1 || stride < 1 || pad < 0)
+      fail(FS_ERR_INVALID, "bad conv arguments");
+    if (H + 2 * pad < kh || W + 2 * pad < kw) fail(FS_ERR_INVALID, "conv output would be empty");
+    if (Cin % 64) fail(FS_ERR_UNSUPPORTED, "Cin must be a multiple of 64");
+    if (Cout % 8) fail(FS_ERR_UNSUPPORTED, "Cout must be a multiple of 8");
+    const int Ho = (H + 2 * pad - kh) / stride + 1, Wo = (W + 2 * pad - kw) / stride + 1;
+    if ((int64_t)B * H * W * Cin * 2 >= (int64_t(1) << 31) || (int64_t)B * Ho * Wo * Cout * 2 >= (int64_t(1) << 31))
+      fail(FS_ERR_UNSUPPORTED, "tensor exceeds 2 GiB");
+    int dev = 0;
+    HIPCHK(hipGetDevice(&dev));
+    ConvArgs a{};
+    a.x = d_in; a.w = d_w; a.bias = d_bias; a.res = d_res; a.y = d_out;
+    a.B = B; a.H = H; a.W = W; a.Cin = Cin; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
+    a.kh = kh; a.kw = kw; a.stride = stride; a.pad = pad; a.relu = relu ? 1 : 0;
+    a.K = kh * kw * Cin; a.Kp = a.K; a.M = B * Ho * Wo; a.Z = 1;
+    const int cus = num_cus_of(dev);
+    const int tl = conv_pick_tile(BF16, a, cus);
+    if (tl < 0 || !conv_tile_ok(BF16, tl, a)) fail(FS_ERR_UNSUPPORTED, "no conv kernel takes this shape");
+    if (conv_tile_direct(conv_tile(BF16, tl))) {
+      a.split = conv_split(BF16, a, cus);
+      if (a.split > 1) {
+        if (conv_partial_floats(a) > kNoallocScratchFloats)
+          fail(FS_ERR_UNSUPPORTED, "the split-K partial sums of this shape (" +
+                                       std::to_string(conv_partial_floats(a) * 4) + " bytes) exceed the " +
+                                       std::to_string(FS_NOALLOC_SCRATCH_BYTES) + "-byte scratch array");
+        a.partial = noalloc_scratch(dev);
+      }
+    }
+    launch_conv(a, BF16, tl, static_cast<hipStream_t>(stream));
+    HIPCHK(hipGetLastError());
+  });
+}
 
 fs_status fs_ensemble_create(const fs_ensemble_desc* desc, fs_ensemble** out) {
   if (out) *out = nullptr;

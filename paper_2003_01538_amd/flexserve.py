@@ -132,6 +132,9 @@ SIGNATURES = [
                                                      [_fp, _fp, _i32p, _i32p, ctypes.c_int32]),
     ("fs_bench_conv", ctypes.c_int, [ctypes.c_int32] * 15 + [ctypes.POINTER(ctypes.c_double), _i32p,
                                                          ctypes.c_int32]),
+    ("fs_conv_bf16_device_noalloc", ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                   ctypes.c_int32, _vp, _fp, _vp] + [ctypes.c_int32] * 6 +
+                                                  [_vp, _vp]),
     ("fs_conv_num_tiles", ctypes.c_int32, [ctypes.c_int32]),
     ("fs_conv_tile_name", ctypes.c_char_p, [ctypes.c_int32, ctypes.c_int32]),
 ]
