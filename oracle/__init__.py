@@ -14,7 +14,9 @@ What it follows in the FlexServe paper:
 * the outputs of all models are returned together, per model and per image
   (Fig. 1 caption; Sec. 2.3), and combined (Sec. 2.1) -> ``ensemble``.
 The paper fixes no arithmetic; the readings taken where it is silent are the
-textbook definitions written in ``fso.c``.
+textbook definitions written in ``fso.c``.  Storage points follow the HIP
+path's: a residual block's projection shortcut (``projection_shortcuts``) is
+summed into the block's last conv before that conv's one rounding.
 
 Parity pins for every function live in ``tests/test_oracle_pins.py``.  The
 end-to-end values of the random bf16 networks have no external pin beyond the
@@ -61,6 +63,7 @@ def lib():
         L.fso_preprocess.argtypes = [P, I, I, I, I, I, P, P, I, P]
         L.fso_fold_bn.argtypes = [P, I, I64, P, P, P, I, P, P]
         L.fso_conv2d.argtypes = [P, I, I, I, I, P, P, P, I, I, I, I, I, I, I, P, P]
+        L.fso_conv2d_proj.argtypes = [P, I, I, I, I, P, P, P, I, I, I, P, P, I, I, I, I, I, I, I, I, P, P]
         L.fso_maxpool.argtypes = [P, I, I, I, I, I, I, I, P]
         L.fso_gap.argtypes = [P, I, I, I, I, I, P]
         L.fso_flatten_nchw.argtypes = [P, I, I, I, I, P]
@@ -129,6 +132,44 @@ def conv2d(x, w, bias, stride, pad, relu, res=None, prec="fp32", want_abs=False)
     lib().fso_conv2d(_p(x), B, H, W, Cin, _p(w), _p(_c(bias)), _p(_c(res)), Cout, kh, kw,
                      stride, pad, int(relu), PREC[prec], _p(out), _p(ab))
     return (out, ab) if want_abs else out
+
+
+def conv2d_proj(x, w, bias, stride, pad, relu, x2, w2, bias2, stride2, prec="fp32", want_abs=False):
+    """A block's last conv with its projection shortcut summed in before the
+    one rounding: x [B,H,W,Cin], w [Cout,kh,kw,Cin], x2 [B,H2,W2,C2] (the
+    block input), w2 [Cout,1,1,C2] or [Cout,C2], 1x1 with stride stride2."""
+    x, w, x2 = _c(x), _c(w), _c(x2)
+    w2 = _c(np.asarray(w2).reshape(w.shape[0], -1))
+    B, H, W, Cin = x.shape
+    Cout, kh, kw, _ = w.shape
+    _, H2, W2, C2 = x2.shape
+    Ho, Wo = (H + 2 * pad - kh) // stride + 1, (W + 2 * pad - kw) // stride + 1
+    assert w2.shape[1] == C2 and (Ho - 1) * stride2 < H2 and (Wo - 1) * stride2 < W2
+    out = np.empty((B, Ho, Wo, Cout), F32)
+    ab = np.empty_like(out) if want_abs else None
+    lib().fso_conv2d_proj(_p(x), B, H, W, Cin, _p(w), _p(_c(bias)), _p(x2), H2, W2, C2, _p(w2), _p(_c(bias2)),
+                          stride2, Cout, kh, kw, stride, pad, int(relu), PREC[prec], _p(out), _p(ab))
+    return (out, ab) if want_abs else out
+
+
+def projection_shortcuts(layers):
+    """{projection layer index: the conv that sums it in}.  A projection
+    shortcut is a 1x1 conv without activation and padding whose output is
+    read only as the residual of one later conv (He et al.'s downsample
+    branch); that conv takes its products into its own sum."""
+    readers = {}
+    for i, L in enumerate(layers):
+        readers.setdefault(L["src"], []).append((i, "src"))
+        if L["op"] == "conv" and L.get("res", -1) >= 0:
+            readers.setdefault(L["res"], []).append((i, "res"))
+    out = {}
+    for d, L in enumerate(layers):
+        if L["op"] != "conv" or L["k"] != 1 or L["pad"] != 0 or L["relu"]:
+            continue
+        r = readers.get(d, [])
+        if len(r) == 1 and r[0][1] == "res" and layers[r[0][0]]["op"] == "conv":
+            out[d] = r[0][0]
+    return out
 
 
 def maxpool(x, k, stride, pad):
@@ -229,10 +270,21 @@ def forward_model(layers, x, prec="fp32", prepared=None, keep=False):
     prepared = prepared or prepare_model(layers, prec)
     outs = []
     last = len(layers) - 1
+    proj = projection_shortcuts(layers)
+    folded = {c: d for d, c in proj.items()}
     for i, (L, wb) in enumerate(zip(layers, prepared)):
+        if i in proj:  # summed into its block's last conv, never stored on its own
+            outs.append(None)
+            continue
         src = x if L["src"] < 0 else outs[L["src"]]
         op = L["op"]
-        if op == "conv":
+        if op == "conv" and i in folded:
+            d = folded[i]
+            D = layers[d]
+            x2 = x if D["src"] < 0 else outs[D["src"]]
+            y = conv2d_proj(src, wb[0], wb[1], L["stride"], L["pad"], L["relu"], x2, prepared[d][0],
+                            prepared[d][1], D["stride"], prec)
+        elif op == "conv":
             res = outs[L["res"]] if L.get("res", -1) >= 0 else None
             y = conv2d(src, wb[0], wb[1], L["stride"], L["pad"], L["relu"], res, prec)
         elif op == "maxpool":
@@ -248,6 +300,7 @@ def forward_model(layers, x, prec="fp32", prepared=None, keep=False):
         if not keep and i > 0:
             # free outputs no later layer reads
             needed = {M["src"] for M in layers[i + 1:]} | {M.get("res", -1) for M in layers[i + 1:]}
+            needed |= {layers[d]["src"] for d, c in proj.items() if c > i}
             for j in range(i + 1):
                 if j not in needed and j != i:
                     outs[j] = None

@@ -14,7 +14,9 @@
  *
  *   resize     bilinear, half-pixel centres, no antialias, border clamp
  *   normalise  x = (v/255 - mean_c)/std_c
- *   conv       y = act(sum_{ky,kx,ci} in*w + bias (+ residual)), zero padding
+ *   conv       y = act(sum_{ky,kx,ci} in*w + bias (+ residual)), zero padding;
+ *              a block's projection shortcut (1x1 conv) summed into the
+ *              block's last conv before its one storage point (fso_conv2d_proj)
  *   max pool   max over the taps inside the image
  *   avg pool   mean over all H*W positions
  *   fc         z = b + W f
@@ -27,8 +29,10 @@
  * the GPU path *stores* is rounded to the storage type at that point:
  * prec 0 = fp32, prec 1 = bf16 (round to nearest, ties to even).  The
  * storage points are: the normalised input, each conv output after its full
- * epilogue, the average-pool output, hidden FC outputs, and the weights once
- * after the batch-norm fold.  Logits, probabilities and sums stay fp32.
+ * epilogue (except a projection shortcut, whose sum goes straight into the
+ * block's last conv), the average-pool output, hidden FC outputs, and the
+ * weights once after the batch-norm fold.  Logits, probabilities and sums
+ * stay fp32.
  *
  * Layout: activations are NHWC (batch, row, column, channel), row-major.
  * Parallelism: OpenMP over independent outputs only; each output's
@@ -184,6 +188,66 @@ void fso_conv2d(const float *in, int B, int H, int W, int Cin,
                     int64_t o = (((int64_t)b * Ho + oy) * Wo + ox) * Cout + co;
                     if (res) y += (double)res[o];
                     if (relu && y < 0) y = 0;
+                    out[o] = store(y, prec);
+                    if (absacc) absacc[o] = (float)aabs;
+                }
+            }
+        }
+    }
+}
+
+/* The last conv of a residual block whose shortcut is a projection (a 1x1
+ * conv of the block input with stride s2, no activation; He et al.'s
+ * ResNets, the kind of CNN the ensemble serves): the projection is not
+ * stored on its own; its products join the conv's sum,
+ *   y = store(relu?(sum_{ky,kx,ci} in*w + sum_{c2} in2[b][oy*s2][ox*s2][c2]*w2[co][c2]
+ *                   + bias + bias2)),
+ * in  [B][H][W][Cin], w [Cout][kh][kw][Cin], in2 [B][H2][W2][C2],
+ * w2 [Cout][C2], bias / bias2 [Cout] or NULL.  The main conv's terms are
+ * summed first, then the projection's, in ascending c2.  absacc as in
+ * fso_conv2d (over both sets of products). */
+void fso_conv2d_proj(const float *in, int B, int H, int W, int Cin, const float *w, const float *bias,
+                     const float *in2, int H2, int W2, int C2, const float *w2, const float *bias2, int s2,
+                     int Cout, int kh, int kw, int stride, int pad, int relu, int prec,
+                     float *out, float *absacc)
+{
+    const int Ho = (H + 2 * pad - kh) / stride + 1;
+    const int Wo = (W + 2 * pad - kw) / stride + 1;
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int oy = 0; oy < Ho; ++oy) {
+            for (int ox = 0; ox < Wo; ++ox) {
+                const float *x2 = in2 + (((int64_t)b * H2 + (int64_t)oy * s2) * W2 + (int64_t)ox * s2) * C2;
+                for (int co = 0; co < Cout; ++co) {
+                    double acc = 0.0, aabs = 0.0;
+                    float acc32 = 0.0f;
+                    for (int ky = 0; ky < kh; ++ky) {
+                        int iy = oy * stride - pad + ky;
+                        if (iy < 0 || iy >= H) continue;
+                        for (int kx = 0; kx < kw; ++kx) {
+                            int ix = ox * stride - pad + kx;
+                            if (ix < 0 || ix >= W) continue;
+                            const float *xp = in + (((int64_t)b * H + iy) * W + ix) * Cin;
+                            const float *wp = w + (((int64_t)co * kh + ky) * kw + kx) * Cin;
+                            for (int ci = 0; ci < Cin; ++ci) {
+                                double p = (double)xp[ci] * (double)wp[ci];
+                                acc += p;
+                                aabs += fabs(p);
+                                if (g_acc32) acc32 = acc32 + xp[ci] * wp[ci];
+                            }
+                        }
+                    }
+                    const float *w2p = w2 + (int64_t)co * C2;
+                    for (int c2 = 0; c2 < C2; ++c2) {
+                        double p = (double)x2[c2] * (double)w2p[c2];
+                        acc += p;
+                        aabs += fabs(p);
+                        if (g_acc32) acc32 = acc32 + x2[c2] * w2p[c2];
+                    }
+                    if (g_acc32) acc = acc32;
+                    double y = acc + (bias ? (double)bias[co] : 0.0) + (bias2 ? (double)bias2[co] : 0.0);
+                    if (relu && y < 0) y = 0;
+                    int64_t o = (((int64_t)b * Ho + oy) * Wo + ox) * Cout + co;
                     out[o] = store(y, prec);
                     if (absacc) absacc[o] = (float)aabs;
                 }

@@ -162,6 +162,57 @@ def test_conv_matches_torch_fp64(cfg):
     assert np.max(np.abs(y - t)) <= 1e-6 * max(1.0, np.abs(t).max())
 
 
+@pytest.mark.parametrize("k,stride,s2,H2", [(3, 1, 2, 18), (3, 1, 2, 17), (1, 1, 1, 9), (3, 2, 2, 9), (1, 1, 2, 17)])
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_conv_with_projection_shortcut_matches_torch_fp64(k, stride, s2, H2, prec):
+    # a block's last conv (input t) plus its 1x1 / stride s2 projection of the
+    # block input x2, summed before one rounding, against torch in float64
+    B, Cin, C2, Cout = 2, 8, 6, 5
+    pad = k // 2
+    Hm = (H2 - 1) // s2 + 1  # the projection's output size
+    H = (Hm - 1) * stride + k - 2 * pad  # main conv output Hm x Hm
+    t = rng.standard_normal((B, H, H, Cin)).astype(np.float32)
+    x2 = rng.standard_normal((B, H2, H2, C2)).astype(np.float32)
+    w = rng.standard_normal((Cout, k, k, Cin)).astype(np.float32)
+    w2 = rng.standard_normal((Cout, 1, 1, C2)).astype(np.float32)
+    b, b2 = rng.standard_normal(Cout).astype(np.float32), rng.standard_normal(Cout).astype(np.float32)
+    if prec == "bf16":
+        t, x2, w, w2 = (oracle.round_bf16(v) for v in (t, x2, w, w2))
+    y = oracle.conv2d_proj(t, w, b, stride, pad, 1, x2, w2, b2, s2, prec)
+    T = lambda a: torch.from_numpy(a).double().permute(0, 3, 1, 2)
+    ref = F.conv2d(T(t), T(w), torch.from_numpy(b).double(), stride=stride, padding=pad) + \
+        F.conv2d(T(x2), T(w2), torch.from_numpy(b2).double(), stride=s2)
+    ref = torch.relu(ref).permute(0, 2, 3, 1).float()
+    assert y.shape == tuple(ref.shape)
+    if prec == "fp32":
+        assert np.max(np.abs(y - ref.numpy())) <= 1e-6 * np.abs(ref.numpy()).max()
+    else:  # one rounding of the float64 sum: equal, except a float ulp away from a tie
+        r = ref.bfloat16().float().numpy()
+        assert np.mean(y == r) >= 0.99 and np.all(np.abs(y - r) <= 2.0 ** -7 * np.abs(r) + 1e-30)
+
+
+def test_projection_with_zero_weights_is_the_plain_conv():
+    t = rng.standard_normal((2, 6, 6, 8)).astype(np.float32)
+    x2 = rng.standard_normal((2, 12, 12, 4)).astype(np.float32)
+    w = rng.standard_normal((3, 3, 3, 8)).astype(np.float32)
+    b = rng.standard_normal(3).astype(np.float32)
+    y = oracle.conv2d_proj(t, w, b, 1, 1, 0, x2, np.zeros((3, 4), np.float32), None, 2, "bf16")
+    assert np.array_equal(y, oracle.conv2d(t, w, b, 1, 1, 0, None, "bf16"))
+
+
+def test_projection_shortcuts_of_the_served_networks():
+    # ResNet-18 has a projection at the first block of stages 2-4, ResNet-50
+    # at the first block of every stage (the stage-1 one changes width 64 ->
+    # 256 at stride 1); each feeds the residual of its block's last conv
+    for arch, n in (("resnet18", 3), ("resnet50", 4), ("vgg11", 0), ("tiny", 0)):
+        layers = wl.ARCHS[arch]()
+        pr = oracle.projection_shortcuts(layers)
+        assert len(pr) == n, arch
+        for d, c in pr.items():
+            assert layers[d]["k"] == 1 and not layers[d]["relu"] and layers[c]["res"] == d and c > d
+            assert layers[c]["cout"] == layers[d]["cout"]
+
+
 def test_conv_residual_then_relu_order():
     x = rng.standard_normal((1, 4, 4, 3)).astype(np.float32)
     w = rng.standard_normal((3, 3, 3, 3)).astype(np.float32)
@@ -340,6 +391,16 @@ def _torch_forward(layers, x, prec):
         return t.bfloat16().double() if prec == "bf16" else t
     outs = []
     xt = torch.from_numpy(x).double().permute(0, 3, 1, 2)
+    # a 1x1 conv without activation that only feeds one residual add is
+    # that block's projection shortcut: its sum is added unrounded
+    uses = {}
+    for L in layers:
+        uses[L["src"]] = uses.get(L["src"], 0) + 1
+        if L["op"] == "conv" and L["res"] >= 0:
+            uses[L["res"]] = uses.get(L["res"], 0) + 1
+    proj = {L["res"] for L in layers if L["op"] == "conv" and L["res"] >= 0
+            and layers[L["res"]]["op"] == "conv" and layers[L["res"]]["k"] == 1
+            and not layers[L["res"]]["relu"] and layers[L["res"]]["pad"] == 0 and uses[L["res"]] == 1}
     for i, L in enumerate(layers):
         src = xt if L["src"] < 0 else outs[L["src"]]
         if L["op"] == "conv":
@@ -354,6 +415,9 @@ def _torch_forward(layers, x, prec):
             y = F.conv2d(src, w.permute(0, 3, 1, 2), b, stride=L["stride"], padding=L["pad"])
             if L["res"] >= 0:
                 y = y + outs[L["res"]]
+            if i in proj:
+                outs.append(y)  # unrounded: summed into the block's last conv
+                continue
             y = st(torch.relu(y) if L["relu"] else y)
         elif L["op"] == "maxpool":
             y = F.max_pool2d(src, L["k"], L["stride"], L["pad"])
