@@ -61,6 +61,8 @@ def parse():
                          "only device-resident passes run, as in a kernel-trace profile")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
+    ap.add_argument("--tuning-log", default="",
+                    help="write the tile tuner's candidate timings (fs_tuning_log) to this file")
     return ap.parse_args()
 
 
@@ -165,6 +167,10 @@ def serve_bench(args):
     for h in handles:
         for b in [Bm] + list(range(1, Bm)):
             h.infer(warm[:b], want_logits=False)
+
+    import gc
+    gc.collect()
+    gc.freeze()
 
     def run_clients(call):
         errs = []
@@ -284,6 +290,14 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.tuning_log:
+        with open(args.tuning_log, "w") as f:
+            f.write(fsb.fs_tuning_log(ens.handle))
+    # everything allocated so far is long-lived: keep it out of the cyclic
+    # garbage collector's full passes, which otherwise land in timed calls
+    import gc
+    gc.collect()
+    gc.freeze()
 
     # plain timing (no events) and event-profiled timing of the same steps
     torch.cuda.synchronize()
@@ -404,6 +418,8 @@ def main():
         "end_to_end": None if args.no_e2e else {
             "images_per_s": round(B / float(np.median(walls)) * 1e3, 1),
             "ms": pct(walls, (("p10", 10), ("p50", 50), ("p90", 90), ("p99", 99))),
+            "in_library_ms": pct(np.sort([sum(p.values()) for p in phases]),
+                                 (("p50", 50), ("p90", 90), ("p99", 99))),
             "phases_ms_median_call": {k: round(v, 4) for k, v in phases[len(phases) // 2].items()},
             "phases_ms_slowest_call": {k: round(v, 4) for k, v in phases[-1].items()},
             "note": "fs_infer from host images to host results, PCIe included"},

@@ -258,6 +258,14 @@ typedef struct {
 fs_status fs_profile_launches(fs_ensemble *e, fs_launch_stat *out, int32_t max_out,
                               int32_t *n_out);
 
+/* The tile tuner's record: one text line per timed candidate (batch
+ * bucket, group, layer, GEMM shape M N K, models Z, K split, tile name, mean
+ * time of one launch in us), for every bucket planned so far.  Copies at
+ * most n - 1 bytes and a terminating zero into buf (when buf is not NULL and
+ * n > 0); *needed (if not NULL) receives the full length + 1.
+ * FS_ERR_INVALID for a NULL handle. */
+fs_status fs_tuning_log(fs_ensemble *e, char *buf, int64_t n, int64_t *needed);
+
 /* Host-side time of the phases of the handle's last fs_infer, in ms,
  * summed over its chunks: ms[0] copying the images into pinned staging
  * memory and issuing their upload, ms[1] issuing the device pass, ms[2]

@@ -46,6 +46,12 @@ struct ConvArgs {
   int K, Kp, M, Z;
   int split = 1;            // K split over workgroups (LDS-DMA kernels only)
   float* partial = nullptr; // split > 1: fp32 partial sums [split][Z][M][Cout]
+  // A residual block's projection shortcut summed into this conv (bf16
+  // LDS-DMA kernels only): reduction indices K1 .. K-1 are the 1x1 conv of
+  // x2 [B][H2][W2][Cin2] at pixel (oy * stride2, ox * stride2), channel
+  // k - K1; the packed weight rows hold both parts.  x2 == null: none.
+  const void* x2 = nullptr; int64_t x2_mstride = 0;
+  int H2 = 0, W2 = 0, Cin2 = 0, stride2 = 1, K1 = 0;
 };
 struct ConvTile {
   int bm, bn, vec;   // block tile and A-load vector (elements)

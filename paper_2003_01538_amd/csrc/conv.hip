@@ -320,6 +320,11 @@ static const ConvTile kTilesBF16[] = {
     {128, 128, 8, "bf16dma1_128x128_w4_v8", 1, 4, 2},
     {128, 64, 8, "bf16dma1_128x64_w4_v8", 1, 4, 2},
     {64, 128, 8, "bf16dma1_64x128_w4_v8", 1, 4, 2},
+    {256, 128, 8, "bf16dma2_256x128_w4_v8", 2, 4, 2},
+    {256, 128, 8, "bf16dma3_256x128_w4_v8", 3, 4, 2},
+    {128, 256, 8, "bf16dma2_128x256_w4_v8", 2, 4, 2},
+    {256, 256, 8, "bf16dma2_256x256_w8_v8", 2, 8, 2},
+    {128, 128, 8, "bf16dma3_128x128_w4_v8", 3, 4, 2},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -338,7 +343,7 @@ bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (c.halo == 2) return p == BF16 && conv_hs_ok(a);
   if (c.halo) return p == BF16 && conv_halo_ok(a, c.th, c.tw, c.bn);
   if (conv_tile_direct(c)) return p == BF16 && conv_dma_ok(a);
-  if (a.split > 1) return false;  // only the LDS-DMA kernels split K
+  if (a.split > 1 || a.x2) return false;  // only the LDS-DMA kernels split K or take a projection
   return a.Cin % c.vec == 0 && a.Kp % CONV_KPAD == 0 && a.Cout % 8 == 0;
 }
 

@@ -237,6 +237,10 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
                                          (uint32_t)((int64_t)a.B * a.H * a.W * a.Cin * 2));
   const __amdgpu_buffer_rsrc_t rw = rsrc(reinterpret_cast<const uint16_t*>(a.w) + z * a.w_mstride,
                                          (uint32_t)((int64_t)a.Cout * a.Kp * 2));
+  // the projection shortcut's input (an empty resource without one)
+  const __amdgpu_buffer_rsrc_t rx2 =
+      rsrc(a.x2 ? reinterpret_cast<const uint16_t*>(a.x2) + z * a.x2_mstride : reinterpret_cast<const uint16_t*>(a.x),
+           a.x2 ? (uint32_t)((int64_t)a.B * a.H2 * a.W2 * a.Cin2 * 2) : 0u);
 
   // lane j of a DMA instruction writes LDS row (j >> 3) of its 8-row block
   // (block i * NW + wave, so row bit 3 is the wave's parity), physical chunk
@@ -248,6 +252,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
   const int dx = (lc * 8) / a.Cin;
 
   int a_off[AP], a_iy[AP], a_ix[AP];
+  uint32_t a2_off[AP];  // projection shortcut: byte offset of (b, oy*s2, ox*s2) + this lane's channels
   const int HoWo = a.Ho * a.Wo;
 #pragma unroll
   for (int i = 0; i < AP; ++i) {
@@ -258,10 +263,12 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
       a_iy[i] = oy * a.stride - a.pad;
       a_ix[i] = ox * a.stride - a.pad;
       a_off[i] = ((b * a.H + a_iy[i]) * a.W + a_ix[i]) * a.Cin + lc * 8;
+      a2_off[i] = (uint32_t)((((int64_t)b * a.H2 + oy * a.stride2) * a.W2 + ox * a.stride2) * a.Cin2 + lc * 8) * 2;
     } else {
       a_iy[i] = -(1 << 28);
       a_ix[i] = 0;
       a_off[i] = 0;
+      a2_off[i] = OOB;
     }
   }
   uint32_t b_off[BP];
@@ -273,17 +280,26 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
 
   auto issue = [&](int kt, int stage) {
     const int k0 = kt * BK;
-    const int tap = k0 / a.Cin;
-    const int ci0 = k0 - tap * a.Cin;
-    const int ky = tap / a.kw, kx = tap - ky * a.kw;
-    const int tap_off = (ky * a.W + kx) * a.Cin + ci0;
     char* base = smem + stage * STAGE;
+    if (a.x2 && k0 >= a.K1) {  // the projection shortcut's 1x1 reduction (wave-uniform)
+      const uint32_t c2 = (uint32_t)(k0 - a.K1) * 2;
 #pragma unroll
-    for (int i = 0; i < AP; ++i) {
-      const int iy = a_iy[i] + ky, ix = a_ix[i] + kx + dx;
-      const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
-      const uint32_t off = ok ? (uint32_t)((a_off[i] + tap_off) * 2) : OOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(base + (i * NW + wave) * 1024), 16, off, 0, 0, 0);
+      for (int i = 0; i < AP; ++i) {
+        const uint32_t off = a2_off[i] == OOB ? OOB : a2_off[i] + c2;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx2, (lds_void*)(base + (i * NW + wave) * 1024), 16, off, 0, 0, 0);
+      }
+    } else {
+      const int tap = k0 / a.Cin;
+      const int ci0 = k0 - tap * a.Cin;
+      const int ky = tap / a.kw, kx = tap - ky * a.kw;
+      const int tap_off = (ky * a.W + kx) * a.Cin + ci0;
+#pragma unroll
+      for (int i = 0; i < AP; ++i) {
+        const int iy = a_iy[i] + ky, ix = a_ix[i] + kx + dx;
+        const bool ok = (unsigned)iy < (unsigned)a.H && (unsigned)ix < (unsigned)a.W;
+        const uint32_t off = ok ? (uint32_t)((a_off[i] + tap_off) * 2) : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(base + (i * NW + wave) * 1024), 16, off, 0, 0, 0);
+      }
     }
 #pragma unroll
     for (int i = 0; i < BP; ++i) {
@@ -1004,7 +1020,11 @@ int conv_split(Prec p, const ConvArgs& a, int num_cus) {
 // Every 64-wide K-tile must lie in one filter row and cover whole pixels.
 bool conv_dma_ok(const ConvArgs& a) {
   const bool tiles_ok = a.Cin % BK == 0 || (a.Cin % 8 == 0 && BK % a.Cin == 0 && (a.kw * a.Cin) % BK == 0);
-  return tiles_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0;
+  // a projection shortcut: whole K-tiles of the main reduction, then of the 1x1 one
+  const bool proj_ok = !a.x2 || (a.K1 % BK == 0 && a.Cin2 % BK == 0 && a.K1 + a.Cin2 == a.K &&
+                                 (a.Ho - 1) * a.stride2 < a.H2 && (a.Wo - 1) * a.stride2 < a.W2 &&
+                                 (int64_t)a.B * a.H2 * a.W2 * a.Cin2 * 2 < (1ll << 31));
+  return tiles_ok && proj_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0;
 }
 
 // Halo kernel shapes: TH output rows x TW (= the output width) pixels, BN
@@ -1012,7 +1032,7 @@ bool conv_dma_ok(const ConvArgs& a) {
 constexpr int HALO_WBYTES = 72 * 1024;
 
 bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn) {
-  return a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin == BK && a.K == a.Kp &&
+  return !a.x2 && a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin == BK && a.K == a.Kp &&
          a.Wo == tw && a.Ho == a.H && a.Wo == a.W && a.Cout % bn == 0 && a.split == 1 &&
          (int64_t)a.Kp * bn * 2 <= HALO_WBYTES && a.Z * (a.Cout / bn) <= 4096;
 }
@@ -1075,6 +1095,11 @@ void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int 
   FS_DMA(128, 128, 2, 2, 1)
   FS_DMA(128, 64, 2, 2, 1)
   FS_DMA(64, 128, 2, 2, 1)
+  FS_DMA(256, 128, 2, 2, 2)
+  FS_DMA(256, 128, 2, 2, 3)
+  FS_DMA(128, 256, 2, 2, 2)
+  FS_DMA(256, 256, 2, 4, 2)
+  FS_DMA(128, 128, 2, 2, 3)
 #undef FS_DMA
 }
 

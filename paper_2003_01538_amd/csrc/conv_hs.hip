@@ -505,7 +505,7 @@ constexpr int HS_NPB[] = {32, 40, 48};  // instantiated patch sizes (8-pixel blo
 }  // namespace
 
 bool conv_hs_ok(const ConvArgs& a) {
-  if (!(a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin % (2 * BK) == 0 && a.K == a.Kp &&
+  if (!(!a.x2 && a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin % (2 * BK) == 0 && a.K == a.Kp &&
         a.Kp == 9 * a.Cin && a.Ho == a.H && a.Wo == a.W && a.Cout % HS_BN == 0))
     return false;
   if ((int64_t)a.B * (a.H + 2) * (a.W + 2) + 1024 >= (1 << 22)) return false;  // fdiv range

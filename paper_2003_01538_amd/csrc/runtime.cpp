@@ -139,6 +139,13 @@ struct LayerPlan {
   bool pool_fused = false;  // conv: also applies the next layer's 3x3/2 max pool, writes the pooled tensor
   bool fused_away = false;  // max pool: done by the conv before it (no launch, shares its slot)
   bool gap_only = false;    // conv whose only reader is the global average pool right after it
+  // projection shortcut (bf16): a 1x1 conv read only as the residual of one
+  // later conv is computed inside that conv's launch as the tail of its
+  // reduction (never stored); proj_into: that conv, on the shortcut;
+  // proj: the shortcut, on the conv, with the shortcut's input
+  int proj_into = -1, proj = -1;
+  int proj_slot = -1, proj_cin = 0, proj_stride = 1;
+  Shape proj_in;
   int kreal = 0;          // kh * kw * cin of the layer as specified (FLOP count)
   int in_c_real = 0;      // input channels as specified (byte count)
 };
@@ -148,6 +155,11 @@ struct Group {
   std::vector<LayerPlan> layers;
   std::vector<int64_t> slot_elems;  // per image, per model
   std::vector<DevBuf> slots;        // [Z][max_batch][slot_elems]
+  // with one stream per group: the group's own stream, end-of-group event
+  // and split-K scratch (groups then run concurrently)
+  hipStream_t stream = nullptr;
+  hipEvent_t done = nullptr;
+  DevBuf conv_partial, fc_partial;
 };
 
 enum KClass { K_PRE = 0, K_CONV, K_MAXPOOL, K_GAP, K_FC, K_SOFTMAX, K_NCLASS };
@@ -258,6 +270,11 @@ struct fs_ensemble {
   HostBuf h_pixels, h_desc, h_out;
   std::unique_ptr<fs::HostPool> pack_pool;  // started by the first fs_infer
   hipStream_t stream = nullptr;
+  // groups on streams of their own, forked after the transformation and
+  // joined before the softmax, so the layers of different groups share the
+  // chip (on by default when there are several groups)
+  bool group_streams = true;
+  hipEvent_t fork = nullptr;
   // end of the last pass, on the stream it ran on: passes share the
   // workspace, so a pass on another stream first waits for this event
   hipEvent_t pass_done = nullptr;
@@ -276,6 +293,8 @@ struct fs_ensemble {
   std::vector<ProfRec> prof;
   std::vector<hipEvent_t> ev_pool;
   int64_t workspace_bytes = 0;
+  // every candidate timing of the tile tuner, one line each (fs_tuning_log)
+  std::string tune_log;
   // host-side phases of the last fs_infer, ms (summed over its chunks)
   double phase_ms[5] = {0, 0, 0, 0, 0};
   // test-only capture of one image's stored layer outputs (fs_debug_capture)
@@ -507,11 +526,33 @@ void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
   g.layers.resize(n);
   std::vector<Shape> out(n);
   std::vector<int> last_use(n, -1);
+  std::vector<int> readers(n, 0);
   for (int i = 0; i < n; ++i) {
     const fs_layer& L = s.layers[i];
     if (L.src >= 0) last_use[L.src] = std::max(last_use[L.src], i);
     if (L.op == FS_OP_CONV && L.residual_src >= 0) last_use[L.residual_src] = std::max(last_use[L.residual_src], i);
+    if (L.src >= 0) ++readers[L.src];
+    if (L.op == FS_OP_CONV && L.residual_src >= 0) ++readers[L.residual_src];
   }
+  // projection shortcuts summed into their block's last conv: a 1x1 conv
+  // (no padding, no ReLU) whose only reader takes it as its residual, both
+  // on 64-channel multiples so that the implicit GEMM runs the two
+  // reductions back to back (bf16 only: in fp32 the shortcut's storage is
+  // exact to fp32 rounding anyway)
+  std::vector<int> proj_of(n, -1), folded_into(n, -1);
+  if (e->prec == BF16)
+    for (int i = 0; i < n; ++i) {
+      const fs_layer& L = s.layers[i];
+      if (L.op != FS_OP_CONV || L.residual_src < 0 || L.src < 0 || L.cin % 64) continue;
+      const int dd = L.residual_src;
+      const fs_layer& D = s.layers[dd];
+      if (D.op != FS_OP_CONV || D.kh != 1 || D.kw != 1 || D.pad != 0 || D.relu || D.src < 0 || D.cin % 64 ||
+          readers[dd] != 1 || D.cout != L.cout)
+        continue;
+      proj_of[i] = dd;
+      folded_into[dd] = i;
+      last_use[D.src] = std::max(last_use[D.src], i);  // read by the conv itself now
+    }
   // slots: greedy reuse of freed buffers
   std::vector<int> slot_busy_until;  // layer index of last reader, per slot
   std::vector<int64_t>& slot_elems = g.slot_elems;
@@ -572,6 +613,23 @@ void plan_group(fs_ensemble* e, const fs_ensemble_desc* d, Group& g) {
     }
     out[i] = P.out;
     P.in_slot = L.src < 0 ? SLOT_INPUT : layer_slot[L.src];
+    if (folded_into[i] >= 0) {  // computed inside its block's last conv: no launch, no tensor
+      P.proj_into = folded_into[i];
+      P.out_slot = -1;
+      continue;
+    }
+    if (proj_of[i] >= 0) {
+      const fs_layer& D = s.layers[proj_of[i]];
+      P.proj = proj_of[i];
+      P.res = -1;
+      P.proj_slot = layer_slot[D.src];
+      P.proj_in = out[D.src];
+      P.proj_cin = D.cin;
+      P.proj_stride = D.stride;
+      P.K += D.cin;
+      P.Kp = (int)round_up(P.K, CONV_KPAD);
+      P.kreal += D.cin;
+    }
     P.res_slot = P.res >= 0 ? layer_slot[P.res] : -1;
     // free slots whose readers are all at or before this layer... but not
     // before this layer has read them: release after assigning the output.
@@ -633,6 +691,7 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   e->pre = d->pre;
   e->device = d->device;
   if (const char* t = std::getenv("FS_TUNE")) e->tune = std::atoi(t) != 0;
+  if (const char* t = std::getenv("FS_GROUP_STREAMS")) e->group_streams = std::atoi(t) != 0;
   // groups of consecutive structurally identical models
   for (int m = 0; m < e->N;) {
     int z = 1;
@@ -650,7 +709,7 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   size_t off = 0;
   for (Group& g : e->groups) {
     for (LayerPlan& P : g.layers) {
-      if (P.op == FS_OP_CONV || P.op == FS_OP_FC) {
+      if ((P.op == FS_OP_CONV && P.proj_into < 0) || P.op == FS_OP_FC) {
         const int64_t welems = P.op == FS_OP_CONV ? (int64_t)P.out.C * P.Kp : (int64_t)P.out.C * P.K;
         P.w_melems = (int64_t)round_up(welems, 128);
         P.b_melems = (int64_t)round_up(P.out.C, 64);
@@ -667,7 +726,7 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   for (Group& g : e->groups) {
     for (int li = 0; li < (int)g.layers.size(); ++li) {
       LayerPlan& P = g.layers[li];
-      if (P.op != FS_OP_CONV && P.op != FS_OP_FC) continue;
+      if ((P.op != FS_OP_CONV || P.proj_into >= 0) && P.op != FS_OP_FC) continue;
       for (int z = 0; z < g.Z; ++z) {
         const fs_layer& L = d->models[g.first + z].layers[li];
         void* wdst = host.data() + P.w_off + (size_t)z * P.w_melems * esz;
@@ -675,6 +734,20 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
         if (P.op == FS_OP_CONV && P.s2d) {
           const std::vector<float> w16 = s2d_weights(L);
           pack_conv(s2d_layer(L, w16), P.cin_p, P.Kp, e->prec, wdst, bdst);
+        } else if (P.op == FS_OP_CONV && P.proj >= 0) {
+          // rows [main conv (K1) | projection shortcut (Cin2)], biases added
+          const fs_layer& D = d->models[g.first + z].layers[P.proj];
+          const int K1 = P.Kp - P.proj_cin;
+          std::vector<char> w1((size_t)P.out.C * K1 * esz), w2((size_t)P.out.C * P.proj_cin * esz);
+          std::vector<float> b1(P.out.C), b2(P.out.C);
+          pack_conv(L, P.cin_p, K1, e->prec, w1.data(), b1.data());
+          pack_conv(D, P.proj_cin, P.proj_cin, e->prec, w2.data(), b2.data());
+          for (int co = 0; co < P.out.C; ++co) {
+            std::memcpy(static_cast<char*>(wdst) + (size_t)co * P.Kp * esz, w1.data() + (size_t)co * K1 * esz, K1 * esz);
+            std::memcpy(static_cast<char*>(wdst) + ((size_t)co * P.Kp + K1) * esz,
+                        w2.data() + (size_t)co * P.proj_cin * esz, P.proj_cin * esz);
+            bdst[co] = b1[co] + b2[co];
+          }
         } else if (P.op == FS_OP_CONV) {
           pack_conv(L, P.cin_p, P.Kp, e->prec, wdst, bdst);
         } else {
@@ -715,13 +788,32 @@ void alloc_workspace(fs_ensemble* e) {
         for (int B = 1; B <= Bm; ++B)
           pf_all = std::max(pf_all, fc_partial_floats(B, P.out.C, fc_pick_split(e->prec, B, P.K, P.out.C, g.Z, e->num_cus), g.Z));
   e->partial.alloc(round_up(std::max<size_t>(pf_all, 1) * 4, 256));
+  if (e->group_streams && e->groups.size() > 1) {
+    // concurrent groups cannot share split-K scratch: one set per group
+    for (Group& g : e->groups) {
+      size_t pf = 0, cf = 0;
+      for (LayerPlan& P : g.layers)
+        for (int B = 1; B <= Bm; ++B) {
+          if (P.op == FS_OP_FC)
+            pf = std::max(pf, fc_partial_floats(B, P.out.C, fc_pick_split(e->prec, B, P.K, P.out.C, g.Z, e->num_cus), g.Z));
+          else if (P.op == FS_OP_CONV && !P.pool_fused && P.proj_into < 0)
+            cf = std::max(cf, conv_partial_floats(conv_args(e, g, P, B, nullptr, 0)));
+        }
+      g.fc_partial.alloc(round_up(std::max<size_t>(pf, 1) * 4, 256));
+      g.conv_partial.alloc(round_up(std::max<size_t>(cf, 1) * 4, 256));
+      ws += g.fc_partial.bytes + g.conv_partial.bytes;
+      HIPCHK(hipStreamCreateWithFlags(&g.stream, hipStreamNonBlocking));
+      HIPCHK(hipEventCreateWithFlags(&g.done, hipEventDisableTiming));
+    }
+    HIPCHK(hipEventCreateWithFlags(&e->fork, hipEventDisableTiming));
+  }
   // split-K scratch of the conv layers, likewise for every batch size: a
   // layer's K split grows as its M shrinks, so a batch below its bucket's
   // size can need more than the bucket size itself
   size_t cf_all = 0;
   for (Group& g : e->groups)
     for (LayerPlan& P : g.layers)
-      if (P.op == FS_OP_CONV && !P.pool_fused)
+      if (P.op == FS_OP_CONV && !P.pool_fused && P.proj_into < 0)
         for (int B = 1; B <= Bm; ++B) cf_all = std::max(cf_all, conv_partial_floats(conv_args(e, g, P, B, nullptr, 0)));
   if (cf_all) e->conv_partial.alloc(round_up(cf_all * 4, 256));
   ws += e->conv_partial.bytes;
@@ -788,8 +880,14 @@ ConvArgs conv_args(fs_ensemble* e, Group& g, const LayerPlan& P, int B, void* y,
   a.Ho = P.out.H; a.Wo = P.out.W; a.Cout = P.out.C;
   a.kh = P.kh; a.kw = P.kw; a.stride = P.stride; a.pad = P.pad; a.relu = P.relu;
   a.K = P.K; a.Kp = P.Kp; a.M = B * P.out.H * P.out.W; a.Z = g.Z;
+  if (P.proj >= 0) {
+    a.x2 = slot_ptr(g, P.proj_slot);
+    a.x2_mstride = (int64_t)g.slot_elems[P.proj_slot] * Bm;
+    a.H2 = P.proj_in.H; a.W2 = P.proj_in.W; a.Cin2 = P.proj_cin; a.stride2 = P.proj_stride;
+    a.K1 = P.Kp - P.proj_cin;
+  }
   a.split = conv_split(e->prec, a, e->num_cus);
-  a.partial = static_cast<float*>(e->conv_partial.p);
+  a.partial = static_cast<float*>(g.conv_partial.p ? g.conv_partial.p : e->conv_partial.p);
   return a;
 }
 
@@ -820,9 +918,11 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
     choice[gi].assign(g.layers.size(), -1);
     for (size_t li = 0; li < g.layers.size(); ++li) {
       LayerPlan& P = g.layers[li];
-      if (P.op != FS_OP_CONV || P.pool_fused) continue;
+      if (P.op != FS_OP_CONV || P.pool_fused || P.proj_into >= 0) continue;
       ConvArgs a = conv_args(e, g, P, bucket, slot_ptr(g, P.out_slot), (int64_t)g.slot_elems[P.out_slot] * e->max_batch);
       const size_t need = conv_partial_floats(a) * 4;
+      if (need > (g.conv_partial.p ? g.conv_partial.bytes : e->conv_partial.bytes))
+        fail(FS_ERR_INTERNAL, "split-K scratch too small for this batch size");
       if (need > e->conv_partial.bytes) {  // split-K scratch for this bucket
         HIPCHK(hipStreamSynchronize(s));
         e->conv_partial.alloc(round_up(need, 256));
@@ -848,6 +948,10 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
           // a later candidate must win by 3%: timing noise alone does not
           // flip the choice between near-equal tiles from run to run
           if (ms < best_ms * 0.97f) { best_ms = ms; best = t; }
+          char line[160];
+          std::snprintf(line, sizeof(line), "bucket %d group %zu layer %zu M %d N %d K %d Z %d split %d tile %s us %.2f\n",
+                        bucket, gi, li, a.M, a.Cout, a.K, a.Z, a.split, conv_tile(e->prec, t).name, ms * 500.0f);
+          e->tune_log += line;
         }
         HIPCHK(hipGetLastError());
       }
@@ -914,8 +1018,15 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
 
   char* arena = static_cast<char*>(e->arena->p);
   const std::vector<std::vector<int>>& tiles = tiles_for(e, B, s);
+  const hipStream_t s_main = s;
+  const bool multi = e->fork != nullptr;
+  if (multi) HIPCHK(hipEventRecord(e->fork, s_main));
   for (size_t gi = 0; gi < e->groups.size(); ++gi) {
     Group& g = e->groups[gi];
+    // the group's launches go to its own stream when groups run concurrently
+    const hipStream_t s = multi ? g.stream : s_main;
+    if (multi) HIPCHK(hipStreamWaitEvent(s, e->fork, 0));
+    launch.s = s;
     bool skip_next = false;  // the layer was done by the launch before it
     for (size_t li = 0; li < g.layers.size(); ++li) {
       LayerPlan& P = g.layers[li];
@@ -940,8 +1051,9 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
       }
       switch (P.op) {
         case FS_OP_CONV: {
+          if (P.proj_into >= 0) break;  // runs inside its block's last conv
           const ConvArgs a = conv_args(e, g, P, B, y, y_ms);
-          if (conv_partial_floats(a) * 4 > e->conv_partial.bytes)  // sized at create for every B
+          if (conv_partial_floats(a) * 4 > (g.conv_partial.p ? g.conv_partial.bytes : e->conv_partial.bytes))
             fail(FS_ERR_INTERNAL, "split-K scratch too small for this batch size");
           const int tile = tiles[gi][li];
           launch.M = a.M; launch.N = a.Cout; launch.K = P.kreal;
@@ -951,7 +1063,8 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           const double in_b = (double)B * P.in.H * P.in.W * P.in_c_real * (P.s2d ? 4 : 1) * esz *
                               (P.in_slot == SLOT_INPUT ? 1 : g.Z);
           const double out_px = P.pool_fused ? (double)B * ((P.out.H - 1) / 2 + 1) * ((P.out.W - 1) / 2 + 1) : a.M;
-          const double bytes = in_b + ((double)a.Cout * kreal * esz + out_px * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
+          const double proj_b = P.proj >= 0 ? (double)B * P.proj_in.elems() * esz * g.Z : 0.0;
+          const double bytes = in_b + proj_b + ((double)a.Cout * kreal * esz + out_px * a.Cout * esz * (a.res ? 2 : 1)) * g.Z;
           const size_t yes = P.last ? 4 : esz;
           if (P.pool_fused) {
             launch(K_CONV, flops, bytes, 1, [&] { launch_conv_stem_pool(a, s); });
@@ -994,7 +1107,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
           a.w = arena + P.w_off; a.w_mstride = P.w_melems;
           a.bias = reinterpret_cast<const float*>(arena + P.b_off); a.b_mstride = P.b_melems;
           a.y = y; a.y_mstride = y_ms;
-          a.partial = static_cast<float*>(e->partial.p);
+          a.partial = static_cast<float*>(g.fc_partial.p ? g.fc_partial.p : e->partial.p);
           a.B = B; a.K = P.K; a.N = P.out.C; a.relu = P.relu; a.out_f32 = P.last ? 1 : 0;
           a.Z = g.Z;
           a.split = fc_pick_split(p, B, a.K, a.N, g.Z, e->num_cus);
@@ -1009,7 +1122,11 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
         }
       }
     }
+    if (multi) HIPCHK(hipEventRecord(g.done, s));
   }
+  launch.s = s_main;
+  if (multi)
+    for (Group& g : e->groups) HIPCHK(hipStreamWaitEvent(s_main, g.done, 0));
 
   launch.group = launch.layer = -1;
   launch.kernel = "";
@@ -1026,7 +1143,7 @@ void run_pass(fs_ensemble* e, const uint8_t* d_pixels, const ImageDesc* d_desc, 
   sa.pos_class = e->pos_class;
   sa.min_votes = e->min_votes;
   const double sbytes = (double)e->N * B * e->C * 8 + (d_mean ? (double)B * e->C * 4 : 0) + B * 4.0;
-  launch(K_SOFTMAX, 0.0, sbytes, 1, [&] { launch_softmax_combine(sa, s); });
+  launch(K_SOFTMAX, 0.0, sbytes, 1, [&] { launch_softmax_combine(sa, s_main); });
   HIPCHK(hipGetLastError());
 }
 
@@ -1042,7 +1159,7 @@ int launches_per_pass(fs_ensemble* e) {
       if (skip_next) { skip_next = false; continue; }
       if (P.op == FS_OP_FC) {
         n += fc_launches(fc_pick_split(e->prec, e->max_batch, P.K, P.out.C, g.Z, e->num_cus));
-      } else if (P.op == FS_OP_CONV) {
+      } else if (P.op == FS_OP_CONV && P.proj_into < 0) {
         const ConvArgs a = conv_args(e, g, P, e->max_batch, nullptr, 0);
         n += (!P.pool_fused && a.split > 1) ? 2 : 1;
         const int gi = (int)(&g - e->groups.data());
@@ -1050,7 +1167,7 @@ int launches_per_pass(fs_ensemble* e) {
         if (P.gap_only && e->prec == BF16 && tile >= 0 && conv_tile_direct(conv_tile(e->prec, tile)) &&
             conv_reduce_gap_ok(a))
           skip_next = true;
-      } else if (!P.fused_away) {
+      } else if (!P.fused_away && P.op != FS_OP_CONV) {
         n += 1;
       }
     }
@@ -1152,6 +1269,12 @@ void destroy_impl(fs_ensemble* e) {
   if (hipSetDevice(e->device) == hipSuccess) {
     if (e->pass_pending) (void)hipEventSynchronize(e->pass_done);
     if (e->pass_done) (void)hipEventDestroy(e->pass_done);
+    for (Group& g : e->groups) {
+      if (g.stream) (void)hipStreamSynchronize(g.stream);
+      if (g.stream) (void)hipStreamDestroy(g.stream);
+      if (g.done) (void)hipEventDestroy(g.done);
+    }
+    if (e->fork) (void)hipEventDestroy(e->fork);
     if (e->stream) (void)hipStreamSynchronize(e->stream);
     clear_graphs(e);
     prof_clear(e);
@@ -1402,6 +1525,7 @@ fs_status fs_ensemble_share(fs_ensemble* src, fs_ensemble** out) {
       e->need_s2d = src->need_s2d;
       e->tiles = src->tiles;
       e->tune = src->tune;
+      e->group_streams = src->group_streams;
       e->graphs = src->graphs;
       set_device(e->device);
       HIPCHK(hipStreamCreateWithFlags(&e->stream, hipStreamNonBlocking));
@@ -1642,6 +1766,21 @@ fs_status fs_profile_launches(fs_ensemble* e, fs_launch_stat* out, int32_t max_o
   });
 }
 
+fs_status fs_tuning_log(fs_ensemble* e, char* buf, int64_t n, int64_t* needed) {
+  if (!e) {
+    g_thread_error = "ensemble is NULL";
+    return FS_ERR_INVALID;
+  }
+  std::lock_guard<std::mutex> lk(e->mu);
+  if (needed) *needed = (int64_t)e->tune_log.size() + 1;
+  if (buf && n > 0) {
+    const size_t k = std::min<size_t>((size_t)n - 1, e->tune_log.size());
+    std::memcpy(buf, e->tune_log.data(), k);
+    buf[k] = 0;
+  }
+  return FS_OK;
+}
+
 fs_status fs_infer_phases(fs_ensemble* e, double* ms) {
   if (!e || !ms) {
     g_thread_error = "ensemble or ms is NULL";
@@ -1686,7 +1825,7 @@ fs_status fs_debug_capture(fs_ensemble* e, int32_t image) {
         e->dbg_have[m].assign(g.layers.size(), 0);
         for (size_t li = 0; li < g.layers.size(); ++li) {
           const LayerPlan& P = g.layers[li];
-          if (P.op == FS_OP_CONV && P.pool_fused) continue;  // only the pooled tensor is stored
+          if (P.op == FS_OP_CONV && (P.pool_fused || P.proj_into >= 0)) continue;  // never stored
           const int64_t elems = P.last ? e->C : P.out.elems();
           e->dbg_off[m][li] = off;
           e->dbg_bytes[m][li] = elems * (int64_t)(P.last ? 4 : esz);

@@ -111,6 +111,7 @@ SIGNATURES = [
     ("fs_profile_read", ctypes.c_int, [_vp, ctypes.POINTER(fs_kernel_stat), ctypes.c_int32, _i32p]),
     ("fs_profile_launches", ctypes.c_int, [_vp, ctypes.POINTER(fs_launch_stat), ctypes.c_int32, _i32p]),
     ("fs_infer_phases", ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
+    ("fs_tuning_log", ctypes.c_int, [_vp, ctypes.c_char_p, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]),
     ("fs_debug_capture", ctypes.c_int, [_vp, ctypes.c_int32]),
     ("fs_debug_layer", ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int32, _fp, ctypes.c_int64]),
     ("fs_test_preprocess", ctypes.c_int, [ctypes.POINTER(fs_image), ctypes.c_int32, ctypes.c_int32,
@@ -362,6 +363,15 @@ def fs_profile_launches(handle, max_out=4096) -> list:
         res.append(dict(kclass=r.kclass.decode(), kernel=r.kernel.decode(), group=r.group, layer=r.layer,
                         M=r.M, N=r.N, K=r.K, Z=r.Z, ms=r.ms, flops=r.flops, bytes=r.bytes))
     return res
+
+
+def fs_tuning_log(handle) -> str:
+    """Every candidate timing of the tile tuner so far, one line each."""
+    need = ctypes.c_int64()
+    _check(load().fs_tuning_log(handle, None, 0, ctypes.byref(need)), handle)
+    buf = ctypes.create_string_buffer(need.value)
+    _check(load().fs_tuning_log(handle, buf, need.value, None), handle)
+    return buf.value.decode()
 
 
 def fs_infer_phases(handle):

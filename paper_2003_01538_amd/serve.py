@@ -186,6 +186,9 @@ def main():
                        max_batch=w["batch"])
     handles = [ens] + [ens.share() for _ in range(args.handles - 1)]
     srv = Server(handles, args.host, args.port, args.max_wait_us, args.policy, args.positive_class, args.min_votes)
+    import gc
+    gc.collect()
+    gc.freeze()  # the models and buffers live as long as the server: no full GC passes over them
     print(f"serving {args.workload} on {srv.url} (POST /infer, GET /health)", flush=True)
     try:
         srv.httpd.serve_forever()

@@ -15,7 +15,10 @@ order of the fp32 sums differs:
 A conv whose max pool or average pool runs inside its launch has no stored
 output; the oracle then runs conv + pool on the stored input, and the bound
 carries through the pool (|max a - max b| <= max |a - b|; an average of
-bounded errors is bounded by their average, plus one rounding).
+bounded errors is bounded by their average, plus one rounding).  A
+projection shortcut computed inside its block's last conv has no stored
+output either: that conv is checked against the oracle's sum of both
+reductions, from the stored block input.
 """
 import numpy as np
 import pytest
@@ -74,7 +77,17 @@ def check_layers(ens, layers, prepared, prec, imgs, image, model, out_hw, exact_
             fused.add(li)
             continue
         src = L["src"]
-        if L["op"] == "conv":
+        if L["op"] == "conv" and L.get("res", -1) in fused:
+            # its projection shortcut ran inside this launch: the oracle sums
+            # both reductions from the stored block input
+            d = L["res"]
+            D = layers[d]
+            o, ab = oracle.conv2d_proj(get(src), prepared[li][0], prepared[li][1], L["stride"], L["pad"],
+                                       L["relu"], get(D["src"]), prepared[d][0], prepared[d][1], D["stride"], prec,
+                                       want_abs=True)
+            _bound_check(y, o, ulp_bf16(o) + 2.0 ** -16 * ab, what + " (with its projection shortcut)", 0.99,
+                         exact_report)
+        elif L["op"] == "conv":
             res = get(L["res"]) if L.get("res", -1) >= 0 else None
             o, ab = oracle.conv2d(get(src), prepared[li][0], prepared[li][1], L["stride"], L["pad"], L["relu"],
                                   res, prec, want_abs=True)
@@ -141,7 +154,7 @@ def test_every_layer_at_full_shapes(wname, images):
             for m, layers in enumerate(w["models"]):
                 checked += check_layers(ens, layers, prepared[m], w["precision"], imgs, image, m, w["out_hw"],
                                         exact)
-            assert checked >= sum(len(L) for L in w["models"]) - 2 * len(w["models"])
+            assert checked >= sum(len(L) - 2 - len(oracle.projection_shortcuts(L)) for L in w["models"])
         fsb.fs_debug_capture(ens.handle, -1)
     worst = min(exact, key=lambda t: t[1])
     print(f"{wname}: {len(exact)} layer checks, lowest bit-identical fraction {worst[1]:.4f} ({worst[0]})")
