@@ -61,6 +61,9 @@ def parse():
                          "only device-resident passes run, as in a kernel-trace profile")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-launch events (no roofline)")
+    ap.add_argument("--max-batch", type=int, default=0,
+                    help="ensemble max_batch (default: the workload's batch); a smaller one runs each step as "
+                         "ceil(B / max_batch) device passes (micro-batches)")
     ap.add_argument("--tuning-log", default="",
                     help="write the tile tuner's candidate timings (fs_tuning_log) to this file")
     return ap.parse_args()
@@ -257,8 +260,9 @@ def main():
     w = wl.workload(args.workload)
     B = w["batch"]
     imgs = list(wl.images_uniform(w["image_seed"], B, *w["in_hw"]))
+    Bm = min(args.max_batch or B, B)
     ens = fsb.Ensemble(w["models"], w["out_hw"], wl.IMAGENET_MEAN, wl.IMAGENET_STD, w["precision"],
-                       max_batch=B)
+                       max_batch=Bm)
     if args.graphs:
         fsb.fs_graphs_enable(ens.handle, True)
     if args.combine != "mean":
@@ -271,11 +275,13 @@ def main():
     flat, desc = wl.pack_images(imgs)
     d_pix = torch.from_numpy(flat).cuda()
     d_desc = torch.tensor([[o, h | (wd << 32), rs] for o, h, wd, rs in desc], dtype=torch.int64).cuda()
-    d_probs = torch.empty((N, B, C), dtype=torch.float32, device="cuda")
-    d_logits = torch.empty_like(d_probs)
-    d_mean = torch.empty((B, C), dtype=torch.float32, device="cuda")
-    d_vote = torch.empty(B, dtype=torch.int32, device="cuda")
-    d_top1 = torch.empty((N, B), dtype=torch.int32, device="cuda")
+    # one set of outputs per micro-batch (model-major within each)
+    chunks = [(c0, min(Bm, B - c0)) for c0 in range(0, B, Bm)]
+    outs = [(torch.empty((N, nb, C), dtype=torch.float32, device="cuda"),
+             torch.empty((N, nb, C), dtype=torch.float32, device="cuda"),
+             torch.empty((nb, C), dtype=torch.float32, device="cuda"),
+             torch.empty(nb, dtype=torch.int32, device="cuda"),
+             torch.empty((N, nb), dtype=torch.int32, device="cuda")) for _, nb in chunks]
     # a stream of our own: the pass runs on it, so events recorded on it
     # bracket the whole pass (stream 0 would hand the pass to the library's
     # own stream)
@@ -283,9 +289,10 @@ def main():
     torch.cuda.synchronize()
 
     def step():
-        fsb.fs_infer_device(ens.handle, d_pix.data_ptr(), d_desc.data_ptr(), B, d_probs.data_ptr(),
-                            d_mean.data_ptr(), d_vote.data_ptr(), d_top1.data_ptr(),
-                            d_logits.data_ptr(), stream.cuda_stream)
+        for (c0, nb), (probs, logits, mean, vote, top1) in zip(chunks, outs):
+            fsb.fs_infer_device(ens.handle, d_pix.data_ptr(), d_desc.data_ptr() + c0 * d_desc.stride(0) * 8, nb,
+                                probs.data_ptr(), mean.data_ptr(), vote.data_ptr(), top1.data_ptr(),
+                                logits.data_ptr(), stream.cuda_stream)
 
     for _ in range(args.warmup):
         step()
@@ -317,7 +324,7 @@ def main():
         torch.cuda.synchronize()
         prof_s = time.perf_counter() - t0
         stats = fsb.fs_profile_read(ens.handle)
-        recs = fsb.fs_profile_launches(ens.handle, max_out=info["launches_per_pass"] * args.steps)
+        recs = fsb.fs_profile_launches(ens.handle, max_out=info["launches_per_pass"] * args.steps * len(chunks))
         per_step = len(recs) // args.steps  # records of one step (a split layer is one record)
         if args.dump_launches:
             with open(args.dump_launches, "w") as f:
@@ -407,7 +414,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w["precision"] == "bf16" else "f32",
         "data": "synthetic: seeded uint8 noise images, He-normal random weights",
-        "config": {"workload": w["name"], "models": list(w["archs"]), "batch": B,
+        "config": {"workload": w["name"], "models": list(w["archs"]), "batch": B, "max_batch": Bm,
                    "input_hw": list(w["in_hw"]), "transformed_hw": list(w["out_hw"]),
                    "combine": args.combine,
                    "flops_per_image": info["flops_per_image"],

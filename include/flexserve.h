@@ -260,7 +260,11 @@ fs_status fs_profile_launches(fs_ensemble *e, fs_launch_stat *out, int32_t max_o
 
 /* The tile tuner's record: one text line per timed candidate (batch
  * bucket, group, layer, GEMM shape M N K, models Z, K split, tile name, mean
- * time of one launch in us), for every bucket planned so far.  Copies at
+ * time of one launch in us) and one "choice" line per timed layer (its
+ * shape key and the tile kept), for every bucket planned so far.  Tiles
+ * come from a committed table of such choices per layer shape and batch
+ * bucket; only layers the table lacks are timed (environment FS_TUNE=1:
+ * time every layer, FS_TUNE=0: never time, the shape rule instead).  Copies at
  * most n - 1 bytes and a terminating zero into buf (when buf is not NULL and
  * n > 0); *needed (if not NULL) receives the full length + 1.
  * FS_ERR_INVALID for a NULL handle. */

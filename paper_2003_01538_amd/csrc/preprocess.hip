@@ -96,8 +96,14 @@ __global__ void __launch_bounds__(256) k_preprocess(PreArgs a) {
   const int oy = pix / a.out_w, ox = pix - oy * a.out_w;
   const ImageTaps it = image_taps(a, a.desc[b]);
   float o[4];
-  transform_pixel(a, it.img, it.row_stride, source_tap(oy, it.h, a.out_h, it.fast_y, it.inv_dy),
-                  source_tap(ox, it.w, a.out_w, it.fast_x, it.inv_dx), o);
+  if (it.h == a.out_h && it.w == a.out_w) {  // same size: the pixel itself, normalised
+    const uint8_t* px = it.img + (int64_t)oy * it.row_stride + 3 * ox;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) o[c] = __builtin_fmaf((float)px[c], 1.0f / 255.0f, -a.mean[c]) * a.inv_std[c];
+  } else {
+    transform_pixel(a, it.img, it.row_stride, source_tap(oy, it.h, a.out_h, it.fast_y, it.inv_dy),
+                    source_tap(ox, it.w, a.out_w, it.fast_x, it.inv_dx), o);
+  }
   o[3] = 0.0f;
   const int64_t idx = ((int64_t)b * a.out_h * a.out_w + pix);
   if (BF16) {
@@ -118,12 +124,32 @@ __global__ void __launch_bounds__(256) k_preprocess_s2d(PreArgs a) {
   if (pix >= hs * ws) return;
   const int Y = pix / ws, X = pix - Y * ws;
   const ImageTaps it = image_taps(a, a.desc[b]);
+  float o[16];
+  if (it.h == a.out_h && it.w == a.out_w) {
+    // same size (uniform over the workgroup): every tap is the pixel itself
+    // with weight 1 (the blend returns it exactly), so only the
+    // normalisation remains
+    const uint8_t* r0 = it.img + (int64_t)(2 * Y) * it.row_stride + 6 * X;
+    const uint8_t* r1 = r0 + it.row_stride;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        const float v = (s < 2 ? r0 : r1)[(s & 1) * 3 + c];
+        o[3 * s + c] = __builtin_fmaf(v, 1.0f / 255.0f, -a.mean[c]) * a.inv_std[c];
+      }
+#pragma unroll
+    for (int e = 12; e < 16; ++e) o[e] = 0.f;
+    uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.out_s2d) + ((int64_t)b * hs * ws + pix) * 16);
+    dst[0] = f8_to_bf8(o);
+    dst[1] = f8_to_bf8(o + 8);
+    return;
+  }
   // the two rows' and the two columns' taps, each shared by two pixels
   const Tap ty[2] = {source_tap(2 * Y, it.h, a.out_h, it.fast_y, it.inv_dy),
                      source_tap(2 * Y + 1, it.h, a.out_h, it.fast_y, it.inv_dy)};
   const Tap tx[2] = {source_tap(2 * X, it.w, a.out_w, it.fast_x, it.inv_dx),
                      source_tap(2 * X + 1, it.w, a.out_w, it.fast_x, it.inv_dx)};
-  float o[16];
 #pragma unroll
   for (int s = 0; s < 4; ++s) transform_pixel(a, it.img, it.row_stride, ty[s >> 1], tx[s & 1], o + 3 * s);
 #pragma unroll

@@ -282,7 +282,9 @@ struct fs_ensemble {
   bool pass_pending = false;
   // conv tile per (batch bucket) -> per group -> per layer, measured once
   std::map<int, std::vector<std::vector<int>>> tiles;
-  bool tune = true;
+  // tile choice: 0 = committed table, else the shape rule (no timing);
+  // 1 = time every candidate; 2 (default) = the table, timing what it lacks
+  int tune = 2;
   // captured passes, replayed with one launch: key = batch size, stream and
   // every buffer the pass reads or writes (caller's and the ensemble's own);
   // off by default (eager launches measured faster, see fs_graphs_enable)
@@ -690,7 +692,7 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
   e->max_batch = d->max_batch;
   e->pre = d->pre;
   e->device = d->device;
-  if (const char* t = std::getenv("FS_TUNE")) e->tune = std::atoi(t) != 0;
+  if (const char* t = std::getenv("FS_TUNE")) e->tune = std::atoi(t);
   if (const char* t = std::getenv("FS_GROUP_STREAMS")) e->group_streams = std::atoi(t) != 0;
   // groups of consecutive structurally identical models
   for (int m = 0; m < e->N;) {
@@ -903,13 +905,38 @@ int batch_bucket(int B, int max_batch) {
 // kernel family per layer (the LDS-DMA family when it applies, the
 // register-staged family otherwise): within a family every tile sums each
 // output in the same order, so the choice never changes the results.
+// The committed tile table: layer shape, batch bucket and models per launch
+// -> tile name.
+struct TileEntry {
+  int bucket, prec, kh, kw, stride, pad, cin, cout, h, w, z, proj_cin, proj_stride;
+  const char* tile;
+};
+const TileEntry kTileTable[] = {
+#include "tile_table.inc"
+    {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, nullptr}};
+
+// The table's tile for this layer at this bucket, or -1.
+int table_tile(const fs_ensemble* e, const ConvArgs& a, int bucket) {
+  for (const TileEntry& t : kTileTable) {
+    if (!t.tile) break;
+    if (t.bucket == bucket && t.prec == (e->prec == BF16 ? 1 : 0) && t.kh == a.kh && t.kw == a.kw &&
+        t.stride == a.stride && t.pad == a.pad && t.cin == a.Cin && t.cout == a.Cout && t.h == a.H && t.w == a.W &&
+        t.z == a.Z && t.proj_cin == (a.x2 ? a.Cin2 : 0) && t.proj_stride == (a.x2 ? a.stride2 : 0)) {
+      for (int i = 0; i < conv_num_tiles(e->prec); ++i)
+        if (std::strcmp(conv_tile(e->prec, i).name, t.tile) == 0) return conv_tile_candidate(e->prec, i, a) ? i : -1;
+      return -1;
+    }
+  }
+  return -1;
+}
+
 const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_t s) {
   const int bucket = batch_bucket(B, e->max_batch);
   auto it = e->tiles.find(bucket);
   if (it != e->tiles.end()) return it->second;
   std::vector<std::vector<int>> choice(e->groups.size());
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (e->tune) {
+  if (e->tune) {  // created lazily enough: events are cheap
     HIPCHK(hipEventCreate(&e0));
     HIPCHK(hipEventCreate(&e1));
   }
@@ -933,7 +960,9 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
       for (int t = 0; t < conv_num_tiles(e->prec); ++t)
         if (conv_tile_candidate(e->prec, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(e->prec, t)));
       int best = conv_pick_tile(e->prec, a, e->num_cus);
-      if (e->tune) {
+      const int from_table = e->tune == 1 ? -1 : table_tile(e, a, bucket);
+      if (from_table >= 0) best = from_table;
+      if (e->tune == 1 || (e->tune == 2 && from_table < 0)) {
         float best_ms = 1e30f;
         for (int t = 0; t < conv_num_tiles(e->prec); ++t) {
           if (!conv_tile_candidate(e->prec, t, a) || conv_tile_family(conv_tile(e->prec, t)) != fam) continue;
@@ -954,6 +983,13 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
           e->tune_log += line;
         }
         HIPCHK(hipGetLastError());
+        char line[200];
+        std::snprintf(line, sizeof(line),
+                      "choice bucket %d group %zu layer %zu prec %d kh %d kw %d stride %d pad %d cin %d cout %d "
+                      "h %d w %d z %d proj_cin %d proj_stride %d tile %s\n",
+                      bucket, gi, li, e->prec == BF16 ? 1 : 0, a.kh, a.kw, a.stride, a.pad, a.Cin, a.Cout, a.H, a.W, a.Z,
+                      a.x2 ? a.Cin2 : 0, a.x2 ? a.stride2 : 0, conv_tile(e->prec, best).name);
+        e->tune_log += line;
       }
       if (best < 0) fail(FS_ERR_INTERNAL, "no conv tile fits a planned layer");
       choice[gi][li] = best;
