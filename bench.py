@@ -64,6 +64,10 @@ def parse():
     ap.add_argument("--max-batch", type=int, default=0,
                     help="ensemble max_batch (default: the workload's batch); a smaller one runs each step as "
                          "ceil(B / max_batch) device passes (micro-batches)")
+    ap.add_argument("--cold", action="store_true",
+                    help="before every profiled step, write a 512 MiB buffer on the launch stream so that the step "
+                         "starts with its inputs and weights out of the caches (the per-kernel rates are then cold "
+                         "for the transformation's image reads and the weight reads)")
     ap.add_argument("--tuning-log", default="",
                     help="write the tile tuner's candidate timings (fs_tuning_log) to this file")
     return ap.parse_args()
@@ -315,11 +319,15 @@ def main():
     plain_s = time.perf_counter() - t0
 
     roof, stats = None, {}
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda") if args.cold else None
     if not args.no_profile:
         fsb.fs_profile_enable(ens.handle, True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for _ in range(args.steps):
+        for i in range(args.steps):
+            if flush is not None:
+                with torch.cuda.stream(stream):
+                    flush.fill_(i & 0xff)
             step()
         torch.cuda.synchronize()
         prof_s = time.perf_counter() - t0
@@ -421,6 +429,7 @@ def main():
                    "launches_per_step": info["launches_per_pass"]},
         "roofline": roof,
         "hbm_kernels": hbm,
+        "hbm_kernels_cold": bool(args.cold),
         "device_step_ms": pct(spans),
         "end_to_end": None if args.no_e2e else {
             "images_per_s": round(B / float(np.median(walls)) * 1e3, 1),
