@@ -68,6 +68,9 @@ def parse():
                     help="before every profiled step, write a 512 MiB buffer on the launch stream so that the step "
                          "starts with its inputs and weights out of the caches (the per-kernel rates are then cold "
                          "for the transformation's image reads and the weight reads)")
+    ap.add_argument("--no-vendor-gemm", action="store_true",
+                    help="skip timing the vendor GEMM (torch.bmm, hipBLASLt) on every conv layer's GEMM shape, "
+                         "the reference column vendor_us of roofline.conv_layers")
     ap.add_argument("--tuning-log", default="",
                     help="write the tile tuner's candidate timings (fs_tuning_log) to this file")
     return ap.parse_args()
@@ -96,6 +99,44 @@ def counted_traffic():
     if vals.get("kernel-source-sha256-16", "").split()[0:1] != [conv_source_hash()]:
         return None
     return int(vals["traffic_bytes_per_conv_launch"])
+
+
+def vendor_gemm_us(Z, M, N, K, reps=20):
+    """Event time of torch.bmm (hipBLASLt) for Z GEMMs [M x K] x [K x N] in
+    bf16: the layer's GEMM with its im2col operand already materialised, so
+    only the library's GEMM is timed (a reference, never the product path)."""
+    import torch
+    a = torch.randn(Z, M, K, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(Z, K, N, device="cuda", dtype=torch.bfloat16).contiguous()
+    c = torch.empty(Z, M, N, device="cuda", dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.bmm(a, b, out=c)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        torch.bmm(a, b, out=c)
+    e1.record()
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps * 1e3
+
+
+def vendor_reference(conv_layers, by_layer, peak):
+    """Adds vendor_us / vendor_frac_peak to every conv layer entry."""
+    cache = {}
+    for ent, rs in zip(conv_layers, (rs for _, rs in sorted(by_layer.items()))):
+        M, N, K = ent["MNK"]
+        Z = max(1, round(rs[0]["flops"] / (2.0 * M * N * K)))
+        key = (Z, M, N, K)
+        if key not in cache:
+            cache[key] = vendor_gemm_us(Z, M, N, K)
+        us = cache[key]
+        ent["vendor_us"] = round(us, 2)
+        ent["vendor_frac_peak"] = round(rs[0]["flops"] / (us * 1e-6) / 1e12 / peak, 4)
+    torch.cuda.empty_cache()
+    return {"what": "torch.bmm (hipBLASLt), bf16, on each conv layer's GEMM with the im2col operand materialised "
+                    "(no bias, residual or pooling); reference only",
+            "conv_us_per_step": round(sum(e["us"] for e in conv_layers), 1),
+            "vendor_us_per_step": round(sum(e["vendor_us"] for e in conv_layers), 1)}
 
 
 def omp_threads():
@@ -367,6 +408,8 @@ def main():
                                 "us": round(ms_l * 1e3, 2), "tflops": round(tf, 1), "ai": round(ai, 1),
                                 "attainable": round(att, 1), "frac_peak": round(tf / peak, 4),
                                 "frac_attainable": round(tf / att, 4)})
+        if w["precision"] == "bf16" and not args.no_vendor_gemm:
+            roof["vendor_gemm"] = vendor_reference(conv_layers, by_layer, peak)
         roof["conv_layers"] = conv_layers
         print(json.dumps({"profiled_ms_per_step": prof_s / args.steps * 1e3,
                           "kernels": {k: dict(v, avg_us=v["total_ms"] / v["launches"] * 1e3,

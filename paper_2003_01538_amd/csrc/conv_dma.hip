@@ -136,9 +136,11 @@ __device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int ro
 // Bias, residual, ReLU, bf16 rounding and a 16-byte store follow; with a K
 // split the raw fp32 sums go to the partial buffer instead.
 // mg[i]: the output row m (pixel) this lane holds in block i, or -1.
-template <int FM, int FN>
+// PRE: the residual of this lane's outputs is already in registers, rpre
+// ([i][j][gp / 2], as loaded by load_residual); otherwise rpre is unused.
+template <int FM, int FN, bool PRE = false>
 __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&acc)[FM][FN], const int (&mg)[FM],
-                                                int ncol, int z, int sp, int lane) {
+                                                int ncol, int z, int sp, int lane, const uint4 (&rpre)[FM][FN][2]) {
   const int fq = lane >> 5;
   const float* __restrict__ bias = a.bias + z * a.b_mstride;
   const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
@@ -171,7 +173,12 @@ __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&ac
         v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
         v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
         const int64_t o = (int64_t)m * a.Cout + n;
-        if (res) {
+        if (PRE) {
+          float rr[8];
+          bf8_to_f8(rpre[i][j][gp >> 1], rr);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += rr[e];
+        } else if (res) {
           float rr[8];
           bf8_to_f8(*reinterpret_cast<const uint4*>(res + o), rr);
 #pragma unroll
@@ -186,13 +193,37 @@ __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&ac
   }
 }
 
-template <int FM, int FN>
+template <int FM, int FN, bool PRE>
 __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)[FM][FN], int mrow, int ncol,
-                                              int z, int sp, int lane) {
+                                              int z, int sp, int lane, const uint4 (&rpre)[FM][FN][2]) {
   int mg[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) mg[i] = mrow + i * 32 + (lane & 31);
-  conv_epilogue_m<FM, FN>(a, acc, mg, ncol, z, sp, lane);
+  conv_epilogue_m<FM, FN, PRE>(a, acc, mg, ncol, z, sp, lane, rpre);
+}
+
+// The residual of the outputs this lane stores in conv_epilogue_m (pixel
+// mrow + 32 i + (lane & 31), channels ncol + 32 j + 8 (gp + q) .. + 7),
+// loaded into registers; past M or Cout the buffer reads zeros, which the
+// epilogue never stores.
+template <int FM, int FN>
+__device__ __forceinline__ void load_residual(const ConvArgs& a, int mrow, int ncol, int z, int lane,
+                                              uint4 (&rp)[FM][FN][2]) {
+  const __amdgpu_buffer_rsrc_t rr =
+      rsrc(reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride, (uint32_t)((int64_t)a.M * a.Cout * 2));
+  const int fq = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int m = mrow + i * 32 + (lane & 31);
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int n = ncol + j * 32 + 8 * (2 * h + fq);
+        const uint32_t off = m < a.M && n < a.Cout ? (uint32_t)(((int64_t)m * a.Cout + n) * 2) : OOB;
+        rp[i][j][h] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0));
+      }
+  }
 }
 
 // Tile of workgroup `bid` among tiles * Z * split, XCD-contiguous.
@@ -211,9 +242,13 @@ __device__ __forceinline__ TileCoord tile_coord(const ConvArgs& a, int bid) {
 
 // BM x BN block tile, WGM x WGN waves (wave tile BM/WGM x BN/WGN, multiples
 // of 32), v_mfma_f32_32x32x16_bf16.
-template <int BM, int BN, int WGM, int WGN, int STAGES>
-__global__ void __launch_bounds__(64 * WGM * WGN,
-                                  STAGES == 1 ? 4 : (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
+// PRE: the layer has a residual and does not split K; its residual is
+// loaded into registers before the first operand loads, so the fetch
+// overlaps theirs and the MFMAs instead of following them in the epilogue
+// (the memory-bound 1x1 convolutions with a residual wait on nothing else).
+template <int BM, int BN, int WGM, int WGN, int STAGES, bool PRE>
+__global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
+                                                  : (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
   constexpr int NW = WGM * WGN;
   constexpr int TM = BM / WGM, TN = BN / WGN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -322,6 +357,11 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
     mma_ktile<FM, FN>(As, As + BM * ROW, wm * TM, wn * TN, lane, acc);
   };
 
+  // issued before every operand load: vmcnt counts loads in issue order, so
+  // the waits for the operand tiles below also cover these
+  uint4 rpre[FM][FN][2];
+  if constexpr (PRE) load_residual<FM, FN>(a, m0 + wm * TM, n0 + wn * TN, z, lane, rpre);
+
   // this workgroup's share of the K-tiles (all of them unless split-K)
   const int nk_all = a.Kp / BK;
   const int kb = sp * nk_all / a.split, nk = (sp + 1) * nk_all / a.split - kb;
@@ -350,7 +390,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN,
     }
   }
 
-  conv_epilogue<FM, FN>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane);
+  conv_epilogue<FM, FN, PRE>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane, rpre);
 }
 
 // Direct 3x3 / stride 1 / pad 1 convolution with the input halo staged
@@ -1078,10 +1118,14 @@ void launch_conv_stem_pool(const ConvArgs& a, hipStream_t s) {
 
 void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s) {
   const int tiles = ((a.M + bm - 1) / bm) * ((a.Cout + bn - 1) / bn) * a.Z * a.split;
-#define FS_DMA(BMv, BNv, WMv, WNv, Sv)                                                                   \
-  if (bm == BMv && bn == BNv && waves == WMv * WNv && stages == Sv && wgm == WMv) {                                    \
-    hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
-    return;                                                                                              \
+  const bool pre = a.res && a.split == 1;
+#define FS_DMA(BMv, BNv, WMv, WNv, Sv)                                                                       \
+  if (bm == BMv && bn == BNv && waves == WMv * WNv && stages == Sv && wgm == WMv) {                          \
+    if (pre)                                                                                                 \
+      hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, true>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
+    else                                                                                                     \
+      hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, false>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
+    return;                                                                                                  \
   }
   FS_DMA(128, 128, 2, 2, 2)
   FS_DMA(128, 64, 2, 2, 3)

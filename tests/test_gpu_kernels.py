@@ -125,6 +125,7 @@ CONV_CASES = [
     (1, 4, 70, 128, 128, 3, 1, 1, 1, 1),   # streamed-weight halo with its largest patch (48 blocks)
     (2, 5, 70, 128, 128, 3, 1, 1, 1, 0),   # patch too large for it: the implicit GEMM takes the layer
     (4, 64, 64, 128, 256, 3, 1, 1, 1, 1),  # streamed-weight halo, 256 tiles of 128 x 128
+    (2, 9, 9, 64, 256, 1, 1, 0, 1, 1),     # bottleneck expand, one K-tile (never split): residual prefetched, ragged M
 ]
 # cases the streamed-weight halo kernel (3x3/1, Cin and Cout multiples of 128) fits
 HS_CASES = (5, 10, 11, 12, 13, 14, 16)
