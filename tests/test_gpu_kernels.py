@@ -287,6 +287,8 @@ def test_gap_parity(gpu_lib, prec, shape):
     (5, 2048, 1000, 0, 0),     # ResNet-50 head, ragged batch
     (3, 25088, 64, 1, 1),      # VGG fc1 fan-in (split-K), hidden output
     (70, 4096, 96, 1, 1),      # more than 64 images
+    (32, 4096, 4096, 1, 1),    # VGG fc2: weight-streaming kernel, split-K over 64-feature tiles
+    (17, 1088, 200, 0, 0),     # weight-streaming kernel: a split ending inside a 256-wide chunk, ragged B and N
     (4, 32, 10, 0, 0),         # tiny head
     (1, 512, 1000, 0, 0),
 ])
