@@ -122,6 +122,7 @@ def vendor_gemm_us(Z, M, N, K, reps=20):
 
 def vendor_reference(conv_layers, by_layer, peak):
     """Adds vendor_us / vendor_frac_peak to every conv layer entry."""
+    import torch
     cache = {}
     for ent, rs in zip(conv_layers, (rs for _, rs in sorted(by_layer.items()))):
         M, N, K = ent["MNK"]
