@@ -126,9 +126,11 @@ CONV_CASES = [
     (2, 5, 70, 128, 128, 3, 1, 1, 1, 0),   # patch too large for it: the implicit GEMM takes the layer
     (4, 64, 64, 128, 256, 3, 1, 1, 1, 1),  # streamed-weight halo, 256 tiles of 128 x 128
     (2, 9, 9, 64, 256, 1, 1, 0, 1, 1),     # bottleneck expand, one K-tile (never split): residual prefetched, ragged M
+    (2, 7, 7, 512, 512, 3, 1, 1, 1, 1),    # streamed-weight halo, Cin 512: eight chunks per tile, residual
+    (16, 14, 14, 512, 512, 3, 1, 1, 1, 0),  # streamed-weight halo, 100 tiles over the CUs, tiles across images
 ]
 # cases the streamed-weight halo kernel (3x3/1, Cin and Cout multiples of 128) fits
-HS_CASES = (5, 10, 11, 12, 13, 14, 16)
+HS_CASES = (5, 10, 11, 12, 13, 14, 16, 18, 19)
 
 
 def _conv_inputs(case, prec, seed):
