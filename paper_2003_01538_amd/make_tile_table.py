@@ -8,7 +8,7 @@ The choices become the table the library uses by default (no timing on a
 server's first request of a batch size); the candidate timings are written
 as a summary, the evidence for each choice.
 
-Usage (repository root, GPU machine):
+Usage (repository root, on an MI355X):
   python -m paper_2003_01538_amd.make_tile_table [--summary profiles/conv_tile_choices.md]
 Rebuild the library afterwards (python -m paper_2003_01538_amd.build).
 """
@@ -46,7 +46,7 @@ def main():
 
     entries, seen = [], set()
     summary = ["# Conv tile choices per batch bucket (MI355X, HIP-event timing of every candidate)", "",
-               "Command: `python -m paper_2003_01538_amd.make_tile_table` (repository root, GPU box).", "",
+               "Command: `python -m paper_2003_01538_amd.make_tile_table` (repository root, on an MI355X).", "",
                "Per distinct layer shape and bucket (layers of one shape listed together; layers whose "
                "kernel family has a single tile omitted): the chosen tile and its time per launch, then the "
                "next-best candidate (a later candidate must win by 3 % to be chosen).", ""]

@@ -1,7 +1,7 @@
 """Per-kernel parity of the HIP path against the CPU oracle, element by
 element, on the same seeded inputs (the single-kernel C entry points).
 
-Tolerances (derived from the arithmetic):
+Tolerances (derived from the arithmetic of each kernel):
 * fp32 storage: |gpu - oracle| <= 1e-5 * sum|x*w| + 1e-6 (an fp32 sum in
   another order against a double sum).
 * bf16 storage: |gpu - oracle| <= 1 bf16 ulp of the oracle value +
