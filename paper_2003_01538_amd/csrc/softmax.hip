@@ -132,27 +132,29 @@ __global__ void __launch_bounds__(SM_T) k_softmax_combine(SoftmaxArgs a) {
   }
 }
 
-// Up to 4 models of up to 1024 classes: the models of one image run side by
-// side, 256 threads (4 waves) each, with the same class-to-thread map and
-// the same reductions as above (so the same bits), and meet once in LDS for
-// the combination: S[c] = p_0[c] + p_1[c] + ... in model order.  The chain of
-// dependent steps is one model long instead of N.
-template <int NG>
-__global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a) {
-  constexpr int PER = 4, W = SM_T / 64;  // classes per thread, waves per model
-  __shared__ float ps[NG][PER * SM_T];
+// Up to 8 models of up to 1024 classes: the models of one image run side by
+// side, TPM threads each, and meet once in LDS for the combination: S[c] =
+// p_0[c] + p_1[c] + ... in model order.  The chain of dependent steps is one
+// model long instead of N.  With TPM = 256 (up to 4 models) the class-to-
+// thread map and the reductions are those of the kernel above (so the same
+// bits); 5 to 8 models take TPM = 128 (8 classes per thread, two waves per
+// model), whose sums of exponentials run in another order.
+template <int NG, int TPM = SM_T>
+__global__ void __launch_bounds__(TPM * NG) k_softmax_combine_mg(SoftmaxArgs a) {
+  constexpr int PER = 1024 / TPM, W = TPM / 64;  // classes per thread, waves per model
+  __shared__ float ps[NG][PER * TPM];
   __shared__ float sv[NG * W];
   __shared__ int si[NG * W];
   __shared__ int tops[NG];
   const int b = blockIdx.x, tid = threadIdx.x;
-  const int g = tid / SM_T, t = tid - g * SM_T, lane = tid & 63, wave = tid >> 6;
+  const int g = tid / TPM, t = tid - g * TPM, lane = tid & 63, wave = tid >> 6;
   const bool live = g < a.N;
   const float* row = a.logits + ((int64_t)(live ? g : 0) * a.B + b) * a.C;
   float z[PER], best = -INFINITY;
   int bi = a.C;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    const int c = t + j * SM_T;
+    const int c = t + j * TPM;
     z[j] = (live && c < a.C) ? row[c] : -INFINITY;
     if (live && c < a.C && (z[j] > best || (z[j] == best && c < bi))) { best = z[j]; bi = c; }
   }
@@ -168,7 +170,7 @@ __global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a)
   float e[PER], part = 0.f;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    e[j] = (live && (t + j * SM_T) < a.C) ? expf(z[j] - best) : 0.f;
+    e[j] = (live && (t + j * TPM) < a.C) ? expf(z[j] - best) : 0.f;
     part += e[j];
   }
   part = wave_sum(part);
@@ -181,7 +183,7 @@ __global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a)
   float* prow = a.probs + ((int64_t)(live ? g : 0) * a.B + b) * a.C;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    const int c = t + j * SM_T;
+    const int c = t + j * TPM;
     if (live && c < a.C) {
       const float p = e[j] / d;
       prow[c] = p;
@@ -193,7 +195,7 @@ __global__ void __launch_bounds__(SM_T * NG) k_softmax_combine_mg(SoftmaxArgs a)
   float cb = -INFINITY;
   int ci = a.C;
   const float invn = (float)a.N;
-  for (int c = tid; c < a.C; c += SM_T * NG) {
+  for (int c = tid; c < a.C; c += TPM * NG) {
     float S = 0.f;
     for (int m = 0; m < a.N; ++m) S += ps[m][c];
     if (a.mean) a.mean[(int64_t)b * a.C + c] = S / invn;
@@ -221,6 +223,14 @@ void launch_softmax_combine(const SoftmaxArgs& a, hipStream_t s) {
       case 2: hipLaunchKernelGGL(k_softmax_combine_mg<2>, grid, dim3(SM_T * 2), 0, s, a); return;
       case 3: hipLaunchKernelGGL(k_softmax_combine_mg<3>, grid, dim3(SM_T * 3), 0, s, a); return;
       default: hipLaunchKernelGGL(k_softmax_combine_mg<4>, grid, dim3(SM_T * 4), 0, s, a); return;
+    }
+  }
+  if (per <= 4 && a.N <= 8) {
+    switch (a.N) {
+      case 5: hipLaunchKernelGGL((k_softmax_combine_mg<5, 128>), grid, dim3(128 * 5), 0, s, a); return;
+      case 6: hipLaunchKernelGGL((k_softmax_combine_mg<6, 128>), grid, dim3(128 * 6), 0, s, a); return;
+      case 7: hipLaunchKernelGGL((k_softmax_combine_mg<7, 128>), grid, dim3(128 * 7), 0, s, a); return;
+      default: hipLaunchKernelGGL((k_softmax_combine_mg<8, 128>), grid, dim3(128 * 8), 0, s, a); return;
     }
   }
   if (per <= 1) hipLaunchKernelGGL(k_softmax_combine<1>, grid, block, 0, s, a);

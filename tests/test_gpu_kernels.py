@@ -313,7 +313,8 @@ def test_fc_parity(gpu_lib, prec, B, K, N, relu, out_storage):
 
 # -------------------------------------------------------- softmax + combine
 @pytest.mark.parametrize("N,B,C,scale", [(3, 32, 1000, 80.0), (5, 7, 1000, 3.0), (2, 4, 10, 2.0),
-                                         (1, 3, 4096, 1.0), (4, 2, 257, 0.0)])
+                                         (1, 3, 4096, 1.0), (4, 2, 257, 0.0), (8, 5, 1000, 40.0),
+                                         (7, 3, 129, 1.0)])
 def test_softmax_combine_parity(gpu_lib, N, B, C, scale):
     rng = np.random.default_rng(N * 100 + C)
     z = (rng.standard_normal((N, B, C)) * scale).astype(np.float32)
