@@ -325,6 +325,9 @@ static const ConvTile kTilesBF16[] = {
     {128, 256, 8, "bf16dma2_128x256_w4_v8", 2, 4, 2},
     {256, 256, 8, "bf16dma2_256x256_w8_v8", 2, 8, 2},
     {128, 128, 8, "bf16dma3_128x128_w4_v8", 3, 4, 2},
+    {160, 128, 8, "bf16dma2_160x128_w4m1_v8", 2, 4, 1},
+    {96, 128, 8, "bf16dma2_96x128_w4m1_v8", 2, 4, 1},
+    {96, 128, 8, "bf16dma1_96x128_w4m1_v8", 1, 4, 1},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},

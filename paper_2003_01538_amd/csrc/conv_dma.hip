@@ -1144,6 +1144,9 @@ void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int 
   FS_DMA(128, 256, 2, 2, 2)
   FS_DMA(256, 256, 2, 4, 2)
   FS_DMA(128, 128, 2, 2, 3)
+  FS_DMA(160, 128, 1, 4, 2)
+  FS_DMA(96, 128, 1, 4, 1)
+  FS_DMA(96, 128, 1, 4, 2)
 #undef FS_DMA
 }
 
