@@ -202,8 +202,8 @@ def summarize(trace_csv, pmc_csv, out_path, cmdline):
          "committed table picks for this layer and bucket (`*`), chosen from HIP-event timings inside the "
          "library on the whole network, where a later candidate had to win by 3 %.", ""]
     groups = {}
-    for c, t, p in zip(cs, tr, pm):
-        groups.setdefault((c["workload"], c["B"], c["Z"], c["shape"]), []).append((c, t, p))
+    for c, tdisp, pdisp in zip(cs, tr, pm):
+        groups.setdefault((c["workload"], c["B"], c["Z"], c["shape"]), []).append((c, tdisp, pdisp))
     agree = total = 0
     for (wname, B, Z, shape), items in groups.items():
         H, W, Cin, Cout, k, s, p, relu, res, proj, lays = shape
@@ -232,7 +232,7 @@ def summarize(trace_csv, pmc_csv, out_path, cmdline):
             L.append(f"| {tn}{' (fastest)' if tn == best else ''} | {us:.1f} | {tf:.0f} | {tf / PEAK_TFLOPS:.3f} | "
                      f"{bz:.3f} | {'*' if tn == chosen else ''} |")
         L.append("")
-    L.insert(len(L), f"Table choices within 5 % of the fastest standalone candidate: {agree} of {total}.")
+    L.append(f"Table choices within 5 % of the fastest standalone candidate: {agree} of {total}.")
     with open(out_path, "w") as f:
         f.write("\n".join(L) + "\n")
     print(f"{len(groups)} layer shapes x buckets; table within 5 %: {agree}/{total} -> {out_path}")
