@@ -138,9 +138,12 @@ __device__ __forceinline__ void mma_ktile(const char* As, const char* Bs, int ro
 // mg[i]: the output row m (pixel) this lane holds in block i, or -1.
 // PRE: the residual of this lane's outputs is already in registers, rpre
 // ([i][j][gp / 2], as loaded by load_residual); otherwise rpre is unused.
-template <int FM, int FN, bool PRE = false>
+// BP: the bias of this lane's channels is already in registers, bpre
+// ([j][gp / 2]); otherwise it is read here and bpre is unused.
+template <int FM, int FN, bool PRE = false, bool BP = false>
 __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&acc)[FM][FN], const int (&mg)[FM],
-                                                int ncol, int z, int sp, int lane, const uint4 (&rpre)[FM][FN][2]) {
+                                                int ncol, int z, int sp, int lane, const uint4 (&rpre)[FM][FN][2],
+                                                const float (&bpre)[FN][2][8]) {
   const int fq = lane >> 5;
   const float* __restrict__ bias = a.bias + z * a.b_mstride;
   const uint16_t* __restrict__ res = a.res ? reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride : nullptr;
@@ -168,10 +171,15 @@ __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&ac
           pp[1] = make_float4(v[4], v[5], v[6], v[7]);
           continue;
         }
-        const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
-        const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
-        v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
-        v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+        if (BP) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += bpre[j][gp >> 1][e];
+        } else {
+          const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+          const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+          v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+          v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+        }
         const int64_t o = (int64_t)m * a.Cout + n;
         if (PRE) {
           float rr[8];
@@ -193,13 +201,33 @@ __device__ __forceinline__ void conv_epilogue_m(const ConvArgs& a, floatx16 (&ac
   }
 }
 
-template <int FM, int FN, bool PRE>
+template <int FM, int FN, bool PRE, bool BP>
 __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, floatx16 (&acc)[FM][FN], int mrow, int ncol,
-                                              int z, int sp, int lane, const uint4 (&rpre)[FM][FN][2]) {
+                                              int z, int sp, int lane, const uint4 (&rpre)[FM][FN][2],
+                                              const float (&bpre)[FN][2][8]) {
   int mg[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) mg[i] = mrow + i * 32 + (lane & 31);
-  conv_epilogue_m<FM, FN, PRE>(a, acc, mg, ncol, z, sp, lane, rpre);
+  conv_epilogue_m<FM, FN, PRE, BP>(a, acc, mg, ncol, z, sp, lane, rpre, bpre);
+}
+
+// The bias of the channels this lane stores in conv_epilogue_m (ncol + 32 j
+// + 8 (gp + q) .. + 7 for gp = 0, 2), loaded into registers; channels past
+// Cout (never stored) read the last eight.
+template <int FN>
+__device__ __forceinline__ void load_bias(const ConvArgs& a, int ncol, int z, int lane, float (&bp)[FN][2][8]) {
+  const float* __restrict__ bias = a.bias + z * a.b_mstride;
+  const int fq = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int n = min(ncol + j * 32 + 8 * (2 * h + fq), a.Cout - 8);
+      const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+      const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+      bp[j][h][0] = b0.x; bp[j][h][1] = b0.y; bp[j][h][2] = b0.z; bp[j][h][3] = b0.w;
+      bp[j][h][4] = b1.x; bp[j][h][5] = b1.y; bp[j][h][6] = b1.z; bp[j][h][7] = b1.w;
+    }
 }
 
 // The residual of the outputs this lane stores in conv_epilogue_m (pixel
@@ -361,6 +389,13 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
   // the waits for the operand tiles below also cover these
   uint4 rpre[FM][FN][2];
   if constexpr (PRE) load_residual<FM, FN>(a, m0 + wm * TM, n0 + wn * TN, z, lane, rpre);
+  // Without a residual in registers (and with a ring: the one-stage tiles
+  // keep their registers for occupancy), an unsplit layer's bias is fetched
+  // here too, so the epilogue does not wait for it after the last MFMA.
+  constexpr bool BIASP = !PRE && STAGES > 1;
+  float bpre[FN][2][8];
+  if constexpr (BIASP)
+    if (a.split == 1) load_bias<FN>(a, n0 + wn * TN, z, lane, bpre);
 
   // this workgroup's share of the K-tiles (all of them unless split-K)
   const int nk_all = a.Kp / BK;
@@ -390,7 +425,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
     }
   }
 
-  conv_epilogue<FM, FN, PRE>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane, rpre);
+  conv_epilogue<FM, FN, PRE, BIASP>(a, acc, m0 + wm * TM, n0 + wn * TN, z, sp, lane, rpre, bpre);
 }
 
 // Direct 3x3 / stride 1 / pad 1 convolution with the input halo staged
