@@ -12,13 +12,14 @@ projection shortcut) so that a profiler run can attribute every dispatch:
   summarize  map the dispatches of a kernel trace and of a counter run back
              to the cases and write a markdown summary
 
-Usage (repository root, on an MI355X, export TMPDIR=/tmp):
-  rocprofv3 --kernel-trace --output-format csv -d gpurun_out/tc/trace -o tc -- \
+Usage (repository root, on an MI355X, export TMPDIR=/tmp; OUT is any scratch
+directory):
+  rocprofv3 --kernel-trace --output-format csv -d OUT/trace -o tc -- \
       python3 -m paper_2003_01538_amd.tile_counters run
   rocprofv3 --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE --output-format csv \
-      -d gpurun_out/tc/pmc -o tc -- python3 -m paper_2003_01538_amd.tile_counters run
-  python3 -m paper_2003_01538_amd.tile_counters summarize --trace gpurun_out/tc/trace/tc_kernel_trace.csv \
-      --pmc gpurun_out/tc/pmc/tc_counter_collection.csv --out profiles/conv_tile_counters.md
+      -d OUT/pmc -o tc -- python3 -m paper_2003_01538_amd.tile_counters run
+  python3 -m paper_2003_01538_amd.tile_counters summarize --trace OUT/trace/tc_kernel_trace.csv \
+      --pmc OUT/pmc/tc_counter_collection.csv --out profiles/conv_tile_counters.md
 """
 from __future__ import annotations
 
@@ -252,12 +253,14 @@ def main():
         cs = cases()
         print(len(cs), "cases")
     else:
-        cmd = ["rocprofv3 --kernel-trace --output-format csv -d gpurun_out/tc/trace -o tc -- "
-               "python3 -m paper_2003_01538_amd.tile_counters run",
-               "rocprofv3 --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE --output-format csv "
-               "-d gpurun_out/tc/pmc -o tc -- python3 -m paper_2003_01538_amd.tile_counters run",
-               "python3 -m paper_2003_01538_amd.tile_counters summarize --trace gpurun_out/tc/trace/tc_kernel_trace.csv "
-               "--pmc gpurun_out/tc/pmc/tc_counter_collection.csv --out profiles/conv_tile_counters.md"]
+        def run_cmd(path, what, tail):
+            d, f = os.path.split(path)
+            return f"rocprofv3 {what} --output-format csv -d {d} -o {f.split(tail)[0]} -- " \
+                   "python3 -m paper_2003_01538_amd.tile_counters run"
+        cmd = [run_cmd(args.trace, "--kernel-trace", "_kernel_trace"),
+               run_cmd(args.pmc, "--pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE", "_counter_collection"),
+               f"python3 -m paper_2003_01538_amd.tile_counters summarize --trace {args.trace} --pmc {args.pmc} "
+               f"--out {os.path.relpath(args.out, ROOT) if os.path.isabs(args.out) else args.out}"]
         summarize(args.trace, args.pmc, args.out, cmd)
 
 
