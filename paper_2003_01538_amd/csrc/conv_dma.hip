@@ -317,12 +317,16 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
   int a_off[AP], a_iy[AP], a_ix[AP];
   uint32_t a2_off[AP];  // projection shortcut: byte offset of (b, oy*s2, ox*s2) + this lane's channels
   const int HoWo = a.Ho * a.Wo;
+  // quotients from float reciprocals (fdiv_small) where every dividend is
+  // below 2^22, integer division otherwise
+  const bool small_m = a.M < (1 << 22);
+  const float inv_howo = 1.0f / (float)HoWo, inv_wo = 1.0f / (float)a.Wo;
 #pragma unroll
   for (int i = 0; i < AP; ++i) {
     const int m = m0 + (i * NW + wave) * 8 + lr;
     if (m < a.M) {
-      const int b = m / HoWo, r = m - b * HoWo;
-      const int oy = r / a.Wo, ox = r - oy * a.Wo;
+      const int b = small_m ? fdiv_small(m, inv_howo) : m / HoWo, r = m - b * HoWo;
+      const int oy = small_m ? fdiv_small(r, inv_wo) : r / a.Wo, ox = r - oy * a.Wo;
       a_iy[i] = oy * a.stride - a.pad;
       a_ix[i] = ox * a.stride - a.pad;
       a_off[i] = ((b * a.H + a_iy[i]) * a.W + a_ix[i]) * a.Cin + lc * 8;
@@ -341,6 +345,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
     b_off[i] = n < a.Cout ? (uint32_t)((n * a.Kp + lc * 8) * 2) : OOB;
   }
 
+  const float inv_cin = 1.0f / (float)a.Cin, inv_kw = 1.0f / (float)a.kw;
   auto issue = [&](int kt, int stage) {
     const int k0 = kt * BK;
     char* base = smem + stage * STAGE;
@@ -352,9 +357,10 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rx2, (lds_void*)(base + (i * NW + wave) * 1024), 16, off, 0, 0, 0);
       }
     } else {
-      const int tap = k0 / a.Cin;
+      // k0 < Kp and the tap index stay far below 2^22 (conv_dma_ok)
+      const int tap = __builtin_amdgcn_readfirstlane(fdiv_small(k0, inv_cin));
       const int ci0 = k0 - tap * a.Cin;
-      const int ky = tap / a.kw, kx = tap - ky * a.kw;
+      const int ky = __builtin_amdgcn_readfirstlane(fdiv_small(tap, inv_kw)), kx = tap - ky * a.kw;
       const int tap_off = (ky * a.W + kx) * a.Cin + ci0;
 #pragma unroll
       for (int i = 0; i < AP; ++i) {
@@ -1099,7 +1105,7 @@ bool conv_dma_ok(const ConvArgs& a) {
   const bool proj_ok = !a.x2 || (a.K1 % BK == 0 && a.Cin2 % BK == 0 && a.K1 + a.Cin2 == a.K &&
                                  (a.Ho - 1) * a.stride2 < a.H2 && (a.Wo - 1) * a.stride2 < a.W2 &&
                                  (int64_t)a.B * a.H2 * a.W2 * a.Cin2 * 2 < (1ll << 31));
-  return tiles_ok && proj_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0;
+  return tiles_ok && proj_ok && a.Kp % BK == 0 && a.K == a.Kp && a.Cout % 8 == 0 && a.Kp < (1 << 22);
 }
 
 // Halo kernel shapes: TH output rows x TW (= the output width) pixels, BN

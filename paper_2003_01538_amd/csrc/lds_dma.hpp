@@ -25,6 +25,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
+// floor(n / d) for 0 <= n < 2^22 from inv, the correctly rounded 1 / d:
+// n + 0.5 is exact, the product carries a relative error below 2^-23, and
+// (n + 0.5) / d lies at least 0.5 / d from an integer, so truncating the
+// product gives the quotient exactly.
+__device__ __forceinline__ int fdiv_small(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
+
 // s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
