@@ -52,7 +52,18 @@ struct ConvArgs {
   // k - K1; the packed weight rows hold both parts.  x2 == null: none.
   const void* x2 = nullptr; int64_t x2_mstride = 0;
   int H2 = 0, W2 = 0, Cin2 = 0, stride2 = 1, K1 = 0;
+  // The packed bf16 weights again in MFMA fragment order (conv_frag_order),
+  // for the LDS-DMA tiles that load their weights into registers; null: the
+  // kernels stage the weights through LDS.
+  const void* wf = nullptr; int64_t wf_mstride = 0;
 };
+// Fragment order of packed bf16 conv weights w [Cout][Kp] (Cout % 32 == 0,
+// Kp % 16 == 0): for 32-channel block nb and k16 step s, 64 lanes x 8 values
+// at ((nb * Kp / 16 + s) * 64 + l) * 8, lane l holding w[32 nb + l % 32]
+// [16 s + 8 (l / 32) .. +8]: the operand one v_mfma_f32_32x32x16_bf16 lane
+// takes for those channels and that k16 step.
+void conv_frag_order(const uint16_t* w, int Cout, int Kp, uint16_t* out);
+inline bool conv_frag_wanted(Prec p, int Cout, int Kp) { return p == BF16 && Cout % 32 == 0 && Kp % 16 == 0; }
 struct ConvTile {
   int bm, bn, vec;   // block tile and A-load vector (elements)
   const char* name;

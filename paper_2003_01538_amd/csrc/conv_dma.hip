@@ -33,6 +33,7 @@
 #include "lds_dma.hpp"
 
 #include <algorithm>
+#include <cstring>
 
 namespace fs {
 
@@ -274,7 +275,13 @@ __device__ __forceinline__ TileCoord tile_coord(const ConvArgs& a, int bid) {
 // loaded into registers before the first operand loads, so the fetch
 // overlaps theirs and the MFMAs instead of following them in the epilogue
 // (the memory-bound 1x1 convolutions with a residual wait on nothing else).
-template <int BM, int BN, int WGM, int WGN, int STAGES, bool PRE>
+// BREG (one row of waves, each owning 32 channels, two stages): no wave
+// reads another wave's weights, so the weight operand skips LDS: each wave
+// loads its fragments for the next K-tile straight into registers from the
+// fragment-ordered copy a.wf (one 1 KB load per k16 step) while the current
+// K-tile's MFMAs run.  The operand values and the MFMA order are those of
+// the LDS path, so the sums are bit-identical.
+template <int BM, int BN, int WGM, int WGN, int STAGES, bool PRE, bool BREG>
 __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
                                                   : (STAGES * (BM + BN) * 128 > 80 * 1024) ? 1 : 2) k_conv_dma(ConvArgs a) {
   constexpr int NW = WGM * WGN;
@@ -282,11 +289,12 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int AP = BM / (8 * NW), BP = BN / (8 * NW);  // DMA instructions per wave per tile
   constexpr int LPT = AP + BP;                             // vmcnt units per tile
-  constexpr int STAGE = (BM + BN) * ROW;
+  constexpr int STAGE = (BREG ? BM : BM + BN) * ROW;
   constexpr int SMEM = STAGES * STAGE;
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile");
   static_assert(AP * 8 * NW == BM && BP * 8 * NW == BN, "DMA blocks");
   static_assert(NW % 2 == 0, "the swizzle of a DMA block's rows depends on the wave only");
+  static_assert(!BREG || (WGM == 1 && FN == 1 && STAGES == 2), "register weights: one row of waves, two stages");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -345,6 +353,23 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
     b_off[i] = n < a.Cout ? (uint32_t)((n * a.Kp + lc * 8) * 2) : OOB;
   }
 
+  // BREG: this wave's 32 channels are fragment block nb = (n0 + 32 wn) / 32
+  // of a.wf; k16 step s of it is 1 KB at (nb * Kp / 16 + s) * 1 KB, lane l
+  // reading the 16 bytes at l * 16 (past Cout: out of range, zeros)
+  const int nw0 = n0 + wn * TN;
+  const uint32_t wf_base =
+      BREG && nw0 < a.Cout ? (uint32_t)((int64_t)(nw0 / 32) * (a.Kp / 16) * 1024 + lane * 16) : OOB;
+  const __amdgpu_buffer_rsrc_t rwf =
+      rsrc(BREG && a.wf ? reinterpret_cast<const uint16_t*>(a.wf) + z * a.wf_mstride : reinterpret_cast<const uint16_t*>(a.w),
+           BREG && a.wf ? (uint32_t)((int64_t)a.Cout * a.Kp * 2) : 0u);
+  auto load_wfrag = [&](int kt, uint4 (&v)[4]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const uint32_t off = wf_base == OOB ? OOB : wf_base + (uint32_t)(kt * 4 + s) * 1024u;
+      v[s] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rwf, off, 0, 0));
+    }
+  };
+
   const float inv_cin = 1.0f / (float)a.Cin, inv_kw = 1.0f / (float)a.kw;
   auto issue = [&](int kt, int stage) {
     const int k0 = kt * BK;
@@ -370,6 +395,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(base + (i * NW + wave) * 1024), 16, off, 0, 0, 0);
       }
     }
+    if constexpr (!BREG)
 #pragma unroll
     for (int i = 0; i < BP; ++i) {
       const uint32_t off = b_off[i] == OOB ? OOB : b_off[i] + (uint32_t)(k0 * 2);
@@ -406,7 +432,51 @@ __global__ void __launch_bounds__(64 * WGM * WGN, STAGES == 1 ? (PRE ? 3 : 4)
   // this workgroup's share of the K-tiles (all of them unless split-K)
   const int nk_all = a.Kp / BK;
   const int kb = sp * nk_all / a.split, nk = (sp + 1) * nk_all / a.split - kb;
-  if constexpr (STAGES == 1) {
+  // BREG: A fragments from LDS as in mma_ktile, the weight fragment of k16
+  // step 2 kh + ks from bv
+  auto compute_breg = [&](int stage, const uint4 (&bv)[4]) {
+    const char* As = smem + stage * STAGE;
+    const int fr = lane & 31;
+    int ra[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) ra[i] = wm * TM + i * 32 + fr;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {
+      bf16x8 af[2][FM], bfr[2][FN];
+      const int fq = lane >> 5;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c = (kh * 2 + ks) * 2 + fq;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8*>(As + ra[i] * ROW + ((c ^ swz(ra[i])) << 4));
+        bfr[ks][0] = __builtin_bit_cast(bf16x8, bv[kh * 2 + ks]);
+      }
+      mma_half<FM, FN>(af, bfr, acc);
+    }
+  };
+  if constexpr (BREG) {
+    // two register sets named by the parity of the K-tile (the loop is
+    // unrolled by two), so no copy moves them between K-tiles; the wait
+    // before each barrier covers the A tile and the weight fragments alike
+    uint4 wa[4], wb[4];
+    if (nk > 0) {
+      issue(kb, 0);
+      load_wfrag(kb, wa);
+    }
+    auto step = [&](int kt, const uint4 (&cur)[4], uint4 (&nxt)[4]) {
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      if (kt + 1 < nk) {
+        issue(kb + kt + 1, (kt + 1) & 1);
+        load_wfrag(kb + kt + 1, nxt);
+      }
+      compute_breg(kt & 1, cur);
+    };
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(kt, wa, wb);
+      if (kt + 1 < nk) step(kt + 1, wb, wa);
+    }
+  } else if constexpr (STAGES == 1) {
     // one buffer (for layers of one or a few K-tiles, where a deeper ring
     // only costs occupancy): fetch, wait, compute, and meet again before the
     // next fetch overwrites the buffer
@@ -1157,15 +1227,41 @@ void launch_conv_stem_pool(const ConvArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_stem_pool, dim3(nwg), dim3(64 * STEM_WAVES), 0, s, a);
 }
 
+void conv_frag_order(const uint16_t* w, int Cout, int Kp, uint16_t* out) {
+  const int S = Kp / 16;
+  for (int nb = 0; nb < Cout / 32; ++nb)
+    for (int st = 0; st < S; ++st)
+      for (int l = 0; l < 64; ++l)
+        std::memcpy(out + (((size_t)nb * S + st) * 64 + l) * 8,
+                    w + (size_t)(nb * 32 + (l & 31)) * Kp + 16 * st + 8 * (l >> 5), 16);
+}
+
+// The weights go to registers (BREG) when the tile has one row of waves of
+// 32 channels each and a fragment-ordered copy of the weights exists.
+template <int BMv, int BNv, int WMv, int WNv, int Sv>
+static void launch_dma_t(const ConvArgs& a, int tiles, bool pre, hipStream_t s) {
+  constexpr bool can_breg = WMv == 1 && BNv / WNv == 32 && Sv == 2;
+  if constexpr (can_breg) {
+    if (a.wf && a.Cout % 32 == 0) {
+      if (pre)
+        hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, true, true>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a);
+      else
+        hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, false, true>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a);
+      return;
+    }
+  }
+  if (pre)
+    hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, true, false>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, false, false>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a);
+}
+
 void launch_conv_dma(const ConvArgs& a, int bm, int bn, int waves, int wgm, int stages, hipStream_t s) {
   const int tiles = ((a.M + bm - 1) / bm) * ((a.Cout + bn - 1) / bn) * a.Z * a.split;
   const bool pre = a.res && a.split == 1;
 #define FS_DMA(BMv, BNv, WMv, WNv, Sv)                                                                       \
   if (bm == BMv && bn == BNv && waves == WMv * WNv && stages == Sv && wgm == WMv) {                          \
-    if (pre)                                                                                                 \
-      hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, true>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
-    else                                                                                                     \
-      hipLaunchKernelGGL((k_conv_dma<BMv, BNv, WMv, WNv, Sv, false>), dim3(tiles), dim3(64 * WMv * WNv), 0, s, a); \
+    launch_dma_t<BMv, BNv, WMv, WNv, Sv>(a, tiles, pre, s);                                                  \
     return;                                                                                                  \
   }
   FS_DMA(128, 128, 2, 2, 2)

@@ -133,6 +133,8 @@ struct LayerPlan {
   int K = 0, Kp = 0;
   size_t w_off = 0, b_off = 0;  // bytes into the arena (model 0)
   int64_t w_melems = 0, b_melems = 0;
+  size_t wf_off = 0;      // bf16 conv: the weights again in MFMA fragment order (model 0), if has_wf
+  bool has_wf = false;
   int in_slot = SLOT_INPUT, res_slot = -1, out_slot = -1;
   bool last = false;
   bool s2d = false;       // first conv rewritten on the space-to-depth input
@@ -720,6 +722,14 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
         P.b_off = off;
         off += (size_t)P.b_melems * 4 * g.Z;
         off = round_up(off, 256);
+        // the implicit GEMM's one-row tiles load their weights into
+        // registers from a fragment-ordered copy (the stem's fused kernel
+        // keeps its weights in LDS)
+        P.has_wf = P.op == FS_OP_CONV && !P.pool_fused && conv_frag_wanted(e->prec, P.out.C, P.Kp);
+        if (P.has_wf) {
+          P.wf_off = off;
+          off = round_up(off + (size_t)P.w_melems * esz * g.Z, 256);
+        }
       }
     }
   }
@@ -755,6 +765,9 @@ void build(fs_ensemble* e, const fs_ensemble_desc* d) {
         } else {
           pack_fc(L, P.in, e->prec, wdst, bdst);
         }
+        if (P.has_wf)
+          conv_frag_order(static_cast<const uint16_t*>(wdst), P.out.C, P.Kp,
+                          reinterpret_cast<uint16_t*>(host.data() + P.wf_off + (size_t)z * P.w_melems * esz));
       }
     }
   }
@@ -874,6 +887,7 @@ ConvArgs conv_args(fs_ensemble* e, Group& g, const LayerPlan& P, int B, void* y,
   a.x = P.in_slot == SLOT_INPUT ? (P.s2d ? e->input_s2d.p : e->input.p) : slot_ptr(g, P.in_slot);
   a.x_mstride = P.in_slot == SLOT_INPUT ? 0 : (int64_t)g.slot_elems[P.in_slot] * Bm;
   a.w = arena + P.w_off; a.w_mstride = P.w_melems;
+  if (P.has_wf) { a.wf = arena + P.wf_off; a.wf_mstride = P.w_melems; }
   a.bias = reinterpret_cast<const float*>(arena + P.b_off); a.b_mstride = P.b_melems;
   a.res = P.res_slot >= 0 ? slot_ptr(g, P.res_slot) : nullptr;
   a.res_mstride = P.res_slot >= 0 ? (int64_t)g.slot_elems[P.res_slot] * Bm : 0;
@@ -2011,13 +2025,20 @@ static void run_test_conv(const float* in, int32_t B, int32_t H, int32_t W, int3
     pack_conv(L, gC, Kp, p, wp.data(), bp.data());
     void* dw = t.alloc(wp.size());
     HIPCHK(hipMemcpy(dw, wp.data(), wp.size(), hipMemcpyHostToDevice));
+    void* dwf = nullptr;
+    if (conv_frag_wanted(p, Cout, Kp)) {  // as the ensemble keeps for its bf16 conv layers
+      std::vector<char> wf(wp.size());
+      conv_frag_order(reinterpret_cast<const uint16_t*>(wp.data()), Cout, Kp, reinterpret_cast<uint16_t*>(wf.data()));
+      dwf = t.alloc(wf.size());
+      HIPCHK(hipMemcpy(dwf, wf.data(), wf.size(), hipMemcpyHostToDevice));
+    }
     void* db = t.alloc(Cout * 4);
     HIPCHK(hipMemcpy(db, bp.data(), Cout * 4, hipMemcpyHostToDevice));
     const int64_t no = (int64_t)B * Ho * Wo * Cout;
     void* dr = res ? upload_as(t, res, no, p) : nullptr;
     void* dy = t.alloc(no * es(p));
     ConvArgs a{};
-    a.x = dx; a.w = dw; a.bias = static_cast<const float*>(db); a.res = dr; a.y = dy;
+    a.x = dx; a.w = dw; a.wf = dwf; a.bias = static_cast<const float*>(db); a.res = dr; a.y = dy;
     a.B = B; a.H = gH; a.W = gW; a.Cin = gC; a.Ho = Ho; a.Wo = Wo; a.Cout = Cout;
     a.kh = gk; a.kw = gk; a.stride = gs; a.pad = gp; a.relu = relu ? 1 : 0;
     a.K = K; a.Kp = Kp; a.M = B * Ho * Wo; a.Z = 1;
@@ -2207,14 +2228,18 @@ fs_status fs_bench_conv(int32_t B, int32_t H, int32_t W, int32_t Cin, int32_t Co
     void* db = t.alloc((size_t)Z * Cout * 4);
     void* dr = residual ? t.alloc((size_t)Z * ny * e) : nullptr;
     void* dy = t.alloc((size_t)Z * ny * e);
-    // small finite values everywhere (0x3c00 = 2^-7 in bf16)
+    void* dwf = conv_frag_wanted(p, Cout, Kp) ? t.alloc((size_t)Z * Cout * Kp * e) : nullptr;
+    // small finite values everywhere (0x3c00 = 2^-7 in bf16; constant
+    // weights are their own fragment order)
     HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dx), 0x3c00, nxg * e / 2));
     HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dw), 0x3c00, (size_t)Z * Cout * Kp * e / 2));
+    if (dwf) HIPCHK(hipMemsetD16(reinterpret_cast<hipDeviceptr_t>(dwf), 0x3c00, (size_t)Z * Cout * Kp * e / 2));
     HIPCHK(hipMemset(db, 0, (size_t)Z * Cout * 4));
     if (dr) HIPCHK(hipMemset(dr, 0, (size_t)Z * ny * e));
     ConvArgs a{};
     a.x = dx; a.x_mstride = 0;
     a.w = dw; a.w_mstride = (int64_t)Cout * Kp;
+    a.wf = dwf; a.wf_mstride = (int64_t)Cout * Kp;
     a.bias = static_cast<const float*>(db); a.b_mstride = Cout;
     a.res = dr; a.res_mstride = ny;
     a.y = dy; a.y_mstride = ny;
