@@ -81,7 +81,7 @@ inline bool conv_tile_direct(const ConvTile& c) { return c.dma > 0; }
 // weights, 1 LDS-DMA implicit GEMM, 0 register-staged implicit GEMM.  A layer
 // always runs in the highest family that fits it, and tiles are only ever
 // compared within one family.
-inline int conv_tile_family(const ConvTile& c) { return c.halo == 2 ? 3 : c.halo ? 2 : (c.dma > 0 ? 1 : 0); }
+inline int conv_tile_family(const ConvTile& c) { return c.halo >= 2 ? 3 : c.halo ? 2 : (c.dma > 0 ? 1 : 0); }
 int conv_num_tiles(Prec p);
 const ConvTile& conv_tile(Prec p, int t);
 int conv_pick_tile(Prec p, const ConvArgs& a, int num_cus);
@@ -93,6 +93,8 @@ bool conv_halo_ok(const ConvArgs& a, int th, int tw, int bn);
 bool conv_hs_ok(const ConvArgs& a);      // the streamed-weight halo kernel can run the layer
 bool conv_hs_chosen(const ConvArgs& a);  // ... and is its automatic choice
 void launch_conv_hs(const ConvArgs& a, hipStream_t s);
+bool conv_hr_ok(const ConvArgs& a, int bm);  // ... in its register-weight form, tiles of bm pixels
+void launch_conv_hr(const ConvArgs& a, int bm, hipStream_t s);
 // Space-to-depth ResNet stem (4x4/1/p2 on 16 channels, 64 outputs, ReLU)
 // fused with the following 3x3/2/p1 max pool; y receives the pooled tensor.
 bool conv_stem_pool_ok(const ConvArgs& a);

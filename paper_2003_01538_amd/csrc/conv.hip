@@ -328,6 +328,8 @@ static const ConvTile kTilesBF16[] = {
     {160, 128, 8, "bf16dma2_160x128_w4m1_v8", 2, 4, 1},
     {96, 128, 8, "bf16dma2_96x128_w4m1_v8", 2, 4, 1},
     {96, 128, 8, "bf16dma1_96x128_w4m1_v8", 1, 4, 1},
+    {160, 128, 8, "bf16hr_160x128_w4m1_v8", 0, 4, 1, 3},
+    {96, 128, 8, "bf16hr_96x128_w4m1_v8", 0, 4, 1, 3},
 };
 static const ConvTile kTilesF32[] = {
     {64, 64, 4, "f32_64x64_v4"},
@@ -343,6 +345,7 @@ const ConvTile& conv_tile(Prec p, int t) { return p == BF16 ? kTilesBF16[t] : kT
 bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
   if (t < 0 || t >= conv_num_tiles(p)) return false;
   const ConvTile& c = conv_tile(p, t);
+  if (c.halo == 3) return p == BF16 && conv_hr_ok(a, c.bm);
   if (c.halo == 2) return p == BF16 && conv_hs_ok(a);
   if (c.halo) return p == BF16 && conv_halo_ok(a, c.th, c.tw, c.bn);
   if (conv_tile_direct(c)) return p == BF16 && conv_dma_ok(a);
@@ -354,7 +357,7 @@ bool conv_tile_ok(Prec p, int t, const ConvArgs& a) {
 // for the streamed-weight halo kernel).
 bool conv_tile_candidate(Prec p, int t, const ConvArgs& a) {
   if (!conv_tile_ok(p, t, a)) return false;
-  return conv_tile(p, t).halo != 2 || conv_hs_chosen(a);
+  return conv_tile(p, t).halo < 2 || conv_hs_chosen(a);
 }
 
 // Largest useful tile: prefer tiles that keep >= 2 workgroups per CU busy,
@@ -389,6 +392,10 @@ static void launch_t(const ConvArgs& a, hipStream_t s) {
 }
 
 void launch_conv(const ConvArgs& a, Prec p, int tile, hipStream_t s, bool reduce) {
+  if (p == BF16 && conv_tile(p, tile).halo == 3) {
+    launch_conv_hr(a, conv_tile(p, tile).bm, s);
+    return;
+  }
   if (p == BF16 && conv_tile(p, tile).halo == 2) {
     launch_conv_hs(a, s);
     return;

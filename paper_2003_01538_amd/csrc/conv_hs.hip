@@ -502,6 +502,247 @@ int64_t hs_patch_px(const ConvArgs& a) {
 
 constexpr int HS_NPB[] = {32, 40, 48};  // instantiated patch sizes (8-pixel blocks)
 
+// ------------------------------------------------------------------------
+// The same convolution with the weights in registers: one workgroup per tile
+// of BM consecutive output pixels x 128 channels, its four waves in one row
+// (each all BM pixels x 32 channels), so no wave needs another's weights:
+// each loads its fragments of the next tap straight into registers from the
+// fragment-ordered copy (conv_frag_order; one 1 KB load per k16 step) while
+// the current tap's MFMAs run.  The LDS holds only the input patch of a
+// 64-channel chunk, double-buffered: the next chunk's patch loads in nine
+// slices during this chunk's taps, and the workgroup meets once per chunk.
+// At most 80 KB of LDS and 256 VGPRs, so two workgroups share a CU.  Patch
+// geometry and swizzle as above; per output the sum runs over chunks, then
+// taps, then the 64 channels in MFMA order, as above, so the bits are the
+// same.  Every tap waits for its loads to land (the next tap's weights and a
+// ninth of the next patch, issued one tap earlier).
+constexpr int HR_BN = 128;
+constexpr int HR_NW = 4;
+constexpr int HR_NPB[] = {24, 32, 40};  // instantiated patch sizes (8-pixel blocks)
+
+template <int BM>
+int64_t hr_patch_px(const ConvArgs& a) {
+  const int64_t HW = (int64_t)a.H * a.W, PW = a.W + 2, HP = a.H + 2;
+  const int64_t tiles = (a.M + BM - 1) / BM;
+  int64_t need = 0;
+  for (int64_t t = 0; t < tiles; ++t) {
+    const int64_t m0 = t * BM, m1 = std::min<int64_t>(a.M, m0 + BM) - 1;
+    const int64_t R0 = (m0 / HW) * HP + (m0 % HW) / a.W;
+    const int64_t b1 = m1 / HW, y1 = (m1 % HW) / a.W, x1 = (m1 % HW) % a.W;
+    const int64_t q = (b1 * HP + y1 - R0) * PW + x1 + 2 * PW + 2;
+    need = std::max(need, q + 1);
+  }
+  return need;
+}
+
+template <int BM, int NPB>
+__global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
+  constexpr int FM = BM / 32;
+  static_assert(BM % 32 == 0 && NPB % HR_NW == 0, "tile");
+  constexpr int NPBW = NPB / HR_NW;  // patch DMA instructions per wave and chunk
+  constexpr int PATCH = NPB * 1024;
+  __shared__ __attribute__((aligned(1024))) char ps0[PATCH];
+  __shared__ __attribute__((aligned(1024))) char ps1[PATCH];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane >> 3, fr = lane & 31, fq = lane >> 5;
+  const int H = a.H, W = a.W, PW = W + 2, HP = H + 2, HW = H * W;
+  const int CH = a.Cin / BK;  // 64-channel chunks (even)
+  const float inv_hw = 1.0f / (float)HW, inv_w = 1.0f / (float)W, inv_pw = 1.0f / (float)PW,
+              inv_hp = 1.0f / (float)HP;
+
+  // ---- tile: N tiles vary fastest, XCD-contiguous
+  const int tiles_m = (a.M + BM - 1) / BM, NT = a.Cout / HR_BN;
+  const int id = xcd_remap(blockIdx.x, tiles_m * NT * a.Z);
+  const int nt = id % NT, mz = id / NT, mt = mz % tiles_m, z = mz / tiles_m;
+  const int m0 = mt * BM, n0 = nt * HR_BN, nw = n0 + wave * 32;
+
+  const __amdgpu_buffer_rsrc_t rx = rsrc(reinterpret_cast<const uint16_t*>(a.x) + z * a.x_mstride,
+                                         (uint32_t)((int64_t)a.B * HW * a.Cin * 2));
+  const __amdgpu_buffer_rsrc_t rwf = rsrc(reinterpret_cast<const uint16_t*>(a.wf) + z * a.wf_mstride,
+                                          (uint32_t)((int64_t)a.Cout * a.Kp * 2));
+  const __amdgpu_buffer_rsrc_t ry = rsrc(reinterpret_cast<uint16_t*>(a.y) + z * a.y_mstride,
+                                         (uint32_t)((int64_t)a.M * a.Cout * 2));
+  const bool has_res = a.res != nullptr;
+  const __amdgpu_buffer_rsrc_t rr =
+      has_res ? rsrc(reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride, (uint32_t)((int64_t)a.M * a.Cout * 2))
+              : rsrc(a.y, 0u);
+
+  // ---- this lane's pixels m = m0 + 32 i + fr: top-left patch position q0,
+  // swizzle key h0 = m, output row mg (-1 past M)
+  const int b0 = fdiv(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv(r0, inv_w);
+  const int R0 = b0 * HP + y0;  // padded row above the first pixel
+  // (the swizzle key and the output row are m itself, 0 / none past M)
+  int q0[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int m = m0 + i * 32 + fr;
+    if (m < a.M) {
+      const int b = fdiv(m, inv_hw), r = m - b * HW, y = fdiv(r, inv_w), x = r - y * W;
+      q0[i] = (b * HP + y - R0) * PW + x;
+    } else {
+      q0[i] = 0;
+    }
+  }
+
+  // ---- weights: tap t of chunk c is K-tile t * CH + c; fragment block of
+  // this wave's 32 channels, k16 step s of that K-tile: 1 KB at
+  // ((nw / 32) * Kp / 16 + 4 kt + s) KB, this lane's 16 bytes at lane * 16
+  const uint32_t wbase = (uint32_t)((int64_t)(nw / 32) * (a.Kp / 16) * 1024 + lane * 16);
+  auto load_w = [&](int kt, uint4 (&v)[4]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      v[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rwf, wbase + (uint32_t)(kt * 4 + k) * 1024u, 0, 0));
+  };
+
+  // ---- patch DMA: instruction v of this wave fills block v * 4 + wave; the
+  // lane's pixel q = block * 8 + lr sits at padded (R0 + q / PW, q % PW)
+  uint32_t po[NPBW];
+#pragma unroll
+  for (int v = 0; v < NPBW; ++v) {
+    const int q = (v * HR_NW + wave) * 8 + lr;
+    const int pr = fdiv(q, inv_pw), pc = q - pr * PW;
+    const int R = R0 + pr;
+    const int b = fdiv(R, inv_hp), yy = R - b * HP - 1, xx = pc - 1;
+    const int lc = (lane & 7) ^ ((((R - 2 * b) * W + pc) >> 1) & 7);
+    const bool ok = b < a.B && (unsigned)yy < (unsigned)H && (unsigned)xx < (unsigned)W;
+    po[v] = ok ? (uint32_t)(((((int64_t)b * H + yy) * W + xx) * a.Cin + lc * 8) * 2) : OOB;
+  }
+  auto issue_slice = [&](auto uc, char* pb, int cc) {
+    constexpr int u = decltype(uc)::value;
+    constexpr int v0 = hs_ps_begin<NPBW>(u), nv = hs_ps<NPBW>(u);
+#pragma unroll
+    for (int v = v0; v < v0 + nv; ++v) {
+      const uint32_t off = po[v] == OOB ? OOB : po[v] + (uint32_t)(cc * BK * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(pb + (v * HR_NW + wave) * 1024), 16, off, 0, 0, 0);
+    }
+  };
+
+  floatx16 acc[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+
+  // one tap: pixel fragments from the patch (row q0 + ky PW + kx, swizzle
+  // key h0 + ky W + kx), weight fragments from wv
+  auto tap_mma = [&](const char* pb, int t, const uint4 (&wv)[4]) {
+    const int ky = t / 3, kx = t - ky * 3;
+    const int dq = ky * PW + kx, dh = ky * W + kx;
+    // (recomputed per tap: the compiler would otherwise keep all 18 taps'
+    // addresses of a chunk pair in registers across the chunk loop)
+    uint32_t pa[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      int q = q0[i], m = m0 + i * 32 + fr;
+      asm volatile("" : "+v"(q), "+v"(m));
+      const int sw = (((m < a.M ? m : 0) + dh) >> 1) & 7;
+      pa[i] = (uint32_t)((q + dq) * ROW) | (uint32_t)((fq ^ sw) << 4);
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      bf16x8 pf[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) pf[i] = *reinterpret_cast<const bf16x8*>(pb + (pa[i] ^ (uint32_t)(kk << 5)));
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wv[kk]), pf[i], acc[i], 0, 0, 0);
+    }
+  };
+
+  // one chunk: nine taps; at tap t the next tap's weights and slice t of
+  // the next chunk's patch are issued, then this tap's MFMAs run, then the
+  // wave waits for what it issued; the workgroup meets after the last tap
+  uint4 wA[4], wB[4];
+  auto chunk = [&](int cc, const char* pcur, char* pnxt, auto par) {
+    constexpr int P0 = decltype(par)::value;  // register set of tap 0: 0 = wA, 1 = wB
+    const bool more = cc + 1 < CH;
+    static_for<0, 9>([&](auto tc) {
+      constexpr int t = decltype(tc)::value;
+      constexpr bool inA = ((P0 + t) & 1) == 0;
+      if (more) issue_slice(tc, pnxt, cc + 1);
+      if (t < 8) {
+        if constexpr (inA) load_w((t + 1) * CH + cc, wB);
+        else load_w((t + 1) * CH + cc, wA);
+      } else if (more) {
+        if constexpr (inA) load_w(cc + 1, wB);
+        else load_w(cc + 1, wA);
+      }
+      if constexpr (inA) tap_mma(pcur, t, wA);
+      else tap_mma(pcur, t, wB);
+      wait_vmcnt<0>();
+    });
+    wg_barrier();
+  };
+
+  // prologue: chunk 0's patch, tap 0's weights
+  static_for<0, 9>([&](auto uc) { issue_slice(uc, ps0, 0); });
+  load_w(0, wA);
+  wait_vmcnt<0>();
+  wg_barrier();
+  for (int cc = 0; cc < CH; cc += 2) {  // chunks in pairs: the patch buffers and register sets by name
+    chunk(cc, ps0, ps1, std::integral_constant<int, 0>{});
+    chunk(cc + 1, ps1, ps0, std::integral_constant<int, 1>{});
+  }
+
+  // ---- epilogue: bias, residual, ReLU, bf16, 16-byte stores (after the
+  // permlane32 swap a lane holds channels nw + 8 (2 h + fq) .. +8 of pixel
+  // m0 + 32 i + fr); the residual and the bias are loaded here, every
+  // register of the loop being taken by the operands
+  uint4 res_v[FM][2];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int m = m0 + i * 32 + fr, n = nw + 8 * (2 * h + fq);
+      const uint32_t off = (has_res && m < a.M) ? (uint32_t)(((int64_t)m * a.Cout + n) * 2) : OOB;
+      res_v[i][h] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0));
+    }
+  float bias_v[2][8];
+  {
+    const float* __restrict__ bias = a.bias + z * a.b_mstride;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int n = nw + 8 * (2 * h + fq);
+      const float4 c0 = *reinterpret_cast<const float4*>(bias + n);
+      const float4 c1 = *reinterpret_cast<const float4*>(bias + n + 4);
+      bias_v[h][0] = c0.x; bias_v[h][1] = c0.y; bias_v[h][2] = c0.z; bias_v[h][3] = c0.w;
+      bias_v[h][4] = c1.x; bias_v[h][5] = c1.y; bias_v[h][6] = c1.z; bias_v[h][7] = c1.w;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int gp = 2 * h;
+      const int mgi = m0 + i * 32 + fr;
+      float v[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][gp * 4 + r]),
+                                                         __float_as_uint(acc[i][(gp + 1) * 4 + r]), false, false);
+        v[r] = __uint_as_float(sw[0]);
+        v[4 + r] = __uint_as_float(sw[1]);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += bias_v[h][e];
+      if (has_res) {
+        float rv[8];
+        bf8_to_f8(res_v[i][h], rv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += rv[e];
+      }
+      if (a.relu)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+      const int n = nw + 8 * (gp + fq);
+      if (mgi < a.M)
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, f8_to_bf8(v)), ry,
+                                               (uint32_t)(((int64_t)mgi * a.Cout + n) * 2), 0, 0);
+    }
+}
+
 }  // namespace
 
 bool conv_hs_ok(const ConvArgs& a) {
@@ -518,7 +759,34 @@ bool conv_hs_ok(const ConvArgs& a) {
 // operand traffic); on wider layers the implicit GEMM's 64 x 128 tiles
 // spread over the CUs better.  Shape-only, so a layer's kernel family, and
 // with it the bits of its results, never depends on the device.
-bool conv_hs_chosen(const ConvArgs& a) { return a.Cin >= 512 && conv_hs_ok(a); }
+bool conv_hs_chosen(const ConvArgs& a) { return a.Cin >= 128 && conv_hs_ok(a); }
+
+// The register-weight form needs the fragment-ordered weights and a patch of
+// at most 40 KB (two buffers per workgroup, two workgroups per CU).
+bool conv_hr_ok(const ConvArgs& a, int bm) {
+  if (!conv_hs_ok(a) || !a.wf) return false;
+  const int64_t need = bm == 160 ? hr_patch_px<160>(a) : bm == 96 ? hr_patch_px<96>(a) : -1;
+  return need >= 0 && need <= 8 * HR_NPB[2];
+}
+
+void launch_conv_hr(const ConvArgs& a_in, int bm, hipStream_t s) {
+  ConvArgs a = a_in;
+  a.split = 1;
+  a.partial = nullptr;
+  const int64_t need = bm == 160 ? hr_patch_px<160>(a) : hr_patch_px<96>(a);
+  int npb = 0;
+  for (int c : HR_NPB)
+    if (need <= 8 * c) { npb = c; break; }
+  const int wgs = ((a.M + bm - 1) / bm) * (a.Cout / HR_BN) * a.Z;
+#define FS_HR(BMv, NPBv)                                                                              \
+  if (bm == BMv && npb == NPBv) {                                                                     \
+    hipLaunchKernelGGL((k_conv_hr<BMv, NPBv>), dim3(wgs), dim3(64 * HR_NW), 0, s, a);                 \
+    return;                                                                                           \
+  }
+  FS_HR(160, 24) FS_HR(160, 32) FS_HR(160, 40)
+  FS_HR(96, 24) FS_HR(96, 32) FS_HR(96, 40)
+#undef FS_HR
+}
 
 void launch_conv_hs(const ConvArgs& a_in, hipStream_t s) {
   ConvArgs a = a_in;  // outputs are always finished here: no K split

@@ -916,9 +916,9 @@ int batch_bucket(int B, int max_batch) {
 // Conv tiles for one batch bucket.  With tuning on, every candidate tile
 // of a layer is timed (HIP events, two launches after a warm-up) on the
 // layer's own buffers and the fastest kept.  Candidates are restricted to one
-// kernel family per layer (the LDS-DMA family when it applies, the
-// register-staged family otherwise): within a family every tile sums each
-// output in the same order, so the choice never changes the results.
+// kernel family per layer (the highest that fits it, a rule on the shape
+// alone): within a family every tile sums each output in the same order, so
+// the choice never changes the results.
 // The committed tile table: layer shape, batch bucket and models per launch
 // -> tile name.
 struct TileEntry {
@@ -929,15 +929,18 @@ const TileEntry kTileTable[] = {
 #include "tile_table.inc"
     {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, nullptr}};
 
-// The table's tile for this layer at this bucket, or -1.
-int table_tile(const fs_ensemble* e, const ConvArgs& a, int bucket) {
+// The table's tile for this layer at this bucket, or -1 (also when the
+// entry names a tile outside the layer's kernel family fam, e.g. a table
+// written under another family rule: the layer is then timed afresh).
+int table_tile(const fs_ensemble* e, const ConvArgs& a, int bucket, int fam) {
   for (const TileEntry& t : kTileTable) {
     if (!t.tile) break;
     if (t.bucket == bucket && t.prec == (e->prec == BF16 ? 1 : 0) && t.kh == a.kh && t.kw == a.kw &&
         t.stride == a.stride && t.pad == a.pad && t.cin == a.Cin && t.cout == a.Cout && t.h == a.H && t.w == a.W &&
         t.z == a.Z && t.proj_cin == (a.x2 ? a.Cin2 : 0) && t.proj_stride == (a.x2 ? a.stride2 : 0)) {
       for (int i = 0; i < conv_num_tiles(e->prec); ++i)
-        if (std::strcmp(conv_tile(e->prec, i).name, t.tile) == 0) return conv_tile_candidate(e->prec, i, a) ? i : -1;
+        if (std::strcmp(conv_tile(e->prec, i).name, t.tile) == 0)
+          return conv_tile_candidate(e->prec, i, a) && conv_tile_family(conv_tile(e->prec, i)) == fam ? i : -1;
       return -1;
     }
   }
@@ -974,7 +977,7 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
       for (int t = 0; t < conv_num_tiles(e->prec); ++t)
         if (conv_tile_candidate(e->prec, t, a)) fam = std::max(fam, conv_tile_family(conv_tile(e->prec, t)));
       int best = conv_pick_tile(e->prec, a, e->num_cus);
-      const int from_table = e->tune == 1 ? -1 : table_tile(e, a, bucket);
+      const int from_table = e->tune == 1 ? -1 : table_tile(e, a, bucket, fam);
       if (from_table >= 0) best = from_table;
       if (e->tune == 1 || (e->tune == 2 && from_table < 0)) {
         float best_ms = 1e30f;

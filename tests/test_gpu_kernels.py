@@ -169,6 +169,7 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
     assert tiles
     ran, ran_names = 0, []
     dma_out = {}  # the LDS-DMA family: every tile sums each output in the same order
+    hs_out = {}   # the streamed-weight halo family (weights through LDS or in registers): likewise
     for t in tiles + [-1]:
         try:
             g = fsb.fs_test_conv(x, w, b, r, s, p, relu, prec, tile=t)
@@ -179,6 +180,8 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
         ran_names.append(fsb.fs_conv_tile_name(prec, t) if t >= 0 else "auto")
         if t >= 0 and "dma" in ran_names[-1]:
             dma_out[ran_names[-1]] = g
+        if t >= 0 and ("hs_" in ran_names[-1] or "hr_" in ran_names[-1]):
+            hs_out[ran_names[-1]] = g
         if prec == BF16:
             assert_bf16_close(g, o, ab, what=f"case {ci} tile {t}")
         else:
@@ -186,11 +189,12 @@ def test_conv_parity_every_tile(gpu_lib, prec, ci):
     assert ran >= 2
     if prec == BF16 and Cin % 64 == 0:  # the LDS-DMA kernels ran on this shape
         assert ran >= 2 + sum(1 for t in tiles if "dma" in fsb.fs_conv_tile_name(prec, t))
-    if dma_out:  # so a tile choice never changes a result: identical bits across the family
-        first_name, first = next(iter(dma_out.items()))
-        for name, g in dma_out.items():
-            assert np.array_equal(g.view(np.uint32), first.view(np.uint32)), \
-                f"case {ci}: {name} differs from {first_name}"
+    for fam in (dma_out, hs_out):  # so a tile choice never changes a result: identical bits across a family
+        if fam:
+            first_name, first = next(iter(fam.items()))
+            for name, g in fam.items():
+                assert np.array_equal(g.view(np.uint32), first.view(np.uint32)), \
+                    f"case {ci}: {name} differs from {first_name}"
     if prec == BF16 and k == 3 and s == 1 and Cin == 64 and Cout % 64 == 0 and W == 56:  # and the halo kernel
         assert any("halo" in n for n in ran_names), ran_names
     if prec == BF16:  # the streamed-weight halo kernel exactly where it fits
