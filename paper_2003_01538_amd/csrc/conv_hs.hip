@@ -1,7 +1,8 @@
 // Direct 3x3 / stride 1 / pad 1 convolution with the input halo staged once
 // per 64-channel chunk and the weights streamed one filter tap at a time, for
 // layers with at least two 64-channel chunks (Cin a multiple of 128) and
-// Cout a multiple of 128.
+// Cout a multiple of 128.  Two kernels: k_conv_hs streams the weights
+// through LDS (below), k_conv_hr holds them in registers (further down).
 //
 // Why: the implicit GEMM fetches every input pixel once per filter tap, so a
 // 3x3 layer moves its input through L2 nine times per output-channel tile.
@@ -754,12 +755,12 @@ bool conv_hs_ok(const ConvArgs& a) {
   return hs_patch_px(a) <= 8 * HS_NPB[2];
 }
 
-// The kernel fits every 3x3/1 layer above, but its 128 x 128 tiles only pay
-// off on deep layers (Cin >= 512: few pixels, the weights dominate the
-// operand traffic); on wider layers the implicit GEMM's 64 x 128 tiles
-// spread over the CUs better.  Shape-only, so a layer's kernel family, and
-// with it the bits of its results, never depends on the device.
-bool conv_hs_chosen(const ConvArgs& a) { return a.Cin >= 128 && conv_hs_ok(a); }
+// The family (the 128 x 128 tiles above and the register-weight form below)
+// takes every 3x3/1 layer it fits: fetching each input pixel once per
+// 64-channel chunk rather than once per tap beats the implicit GEMM there.
+// Shape-only, so a layer's kernel family, and with it the bits of its
+// results, never depends on the device or the batch.
+bool conv_hs_chosen(const ConvArgs& a) { return conv_hs_ok(a); }
 
 // The register-weight form needs the fragment-ordered weights and a patch of
 // at most 40 KB (two buffers per workgroup, two workgroups per CU).

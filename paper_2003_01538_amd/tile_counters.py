@@ -73,19 +73,43 @@ def conv_shapes(models, in_h, in_w):
     return [k + (tuple(v),) for k, v in out.items()]
 
 
-def family_tiles(fsb, shape):
-    """Names of the candidate tiles for a layer shape: the implicit-GEMM
-    (LDS-DMA) family, or [] when the layer runs in a single-tile family (the
-    stem with its pool, the halo kernels)."""
+def patch_px(shape, B, bm):
+    """Patch pixels the halo kernels need for tiles of bm consecutive output
+    pixels (the band of padded rows from above a tile's first pixel through
+    its last pixel's bottom-right tap), as the library computes it."""
+    H, W = shape[0], shape[1]
+    HW, PW, HP, M = H * W, W + 2, H + 2, B * H * W
+    need = 0
+    for m0 in range(0, M, bm):
+        m1 = min(M, m0 + bm) - 1
+        R0 = (m0 // HW) * HP + (m0 % HW) // W
+        b1, y1, x1 = m1 // HW, (m1 % HW) // W, (m1 % HW) % W
+        need = max(need, (b1 * HP + y1 - R0) * PW + x1 + 2 * PW + 2 + 1)
+    return need
+
+
+def family_tiles(fsb, shape, B):
+    """Names of the candidate tiles for a layer shape at batch B: those of
+    the layer's kernel family (the library's shape rule), or [] when the
+    family has a single tile (the stem with its pool, the resident-weight
+    halo kernel)."""
     H, W, Cin, Cout, k, s, p = shape[:7]
+    names = [fsb.fs_conv_tile_name(fsb.FS_BF16, t) for t in range(fsb.fs_conv_num_tiles(fsb.FS_BF16))]
     if Cin == 3:
         return []   # the space-to-depth stem (fused with its max pool)
     if k == 3 and s == 1 and p == 1 and Cin == 64 and W == 56:
         return []   # resident-weight halo kernel
-    if k == 3 and s == 1 and p == 1 and Cin >= 512:
-        return []   # streamed-weight halo kernel
-    n = fsb.fs_conv_num_tiles(fsb.FS_BF16)
-    return [fsb.fs_conv_tile_name(fsb.FS_BF16, t) for t in range(n) if "dma" in fsb.fs_conv_tile_name(fsb.FS_BF16, t)]
+    if k == 3 and s == 1 and p == 1 and Cin % 128 == 0 and Cout % 128 == 0 and not shape[9]:
+        out = []    # streamed-weight halo family: 128-pixel tiles (weights through LDS), 160 and 96 (in registers)
+        for n in names:
+            if "hs_" in n and patch_px(shape, B, 128) <= 8 * 48:
+                out.append(n)
+            elif "hr_160" in n and patch_px(shape, B, 160) <= 8 * 40:
+                out.append(n)
+            elif "hr_96" in n and patch_px(shape, B, 96) <= 8 * 40:
+                out.append(n)
+        return out
+    return [n for n in names if "dma" in n]
 
 
 def cases():
@@ -97,9 +121,8 @@ def cases():
         for shape in conv_shapes(w["models"], *w["out_hw"]):
             if shape[9]:
                 continue  # carries a projection shortcut, which fs_bench_conv does not take
-            tiles = family_tiles(fsb, shape)
             for B in buckets:
-                for tn in tiles:
+                for tn in family_tiles(fsb, shape, B):
                     out.append(dict(workload=wname, B=B, Z=Z, shape=shape, tile=tn))
     return out
 
@@ -175,7 +198,8 @@ def assign(cs, disp):
     out = []
     for i, c in enumerate(cs):
         ds = disp[i * per:(i + 1) * per]
-        if any("k_conv_dma" not in name for name, _ in ds):
+        kern = "k_conv_hr" if "hr_" in c["tile"] else "k_conv_hs" if "hs_" in c["tile"] else "k_conv_dma"
+        if any(kern not in name for name, _ in ds):
             raise SystemExit(f"case {i} ({c['tile']}): unexpected kernel {ds[0][0]}")
         out.append(ds[WARMUP:])
     return out
@@ -191,8 +215,10 @@ def summarize(trace_csv, pmc_csv, out_path, cmdline):
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
     L = ["# Conv tile candidates under rocprofv3: kernel-trace time and matrix-core counters", "",
          "Commands (repository root on an MI355X, `export TMPDIR=/tmp`):", "", "```"] + cmdline + ["```", "",
-         "Every candidate tile of every implicit-GEMM layer shape (layers whose family has a single tile, the "
-         "stem and the halo kernels, are not listed), per batch size, launched alone by `fs_bench_conv` "
+         "Every candidate tile of every conv layer shape whose kernel family has several (the implicit GEMM; "
+         "the streamed-weight halo family of the 3x3/1 layers with Cin >= 128; the stem and the "
+         "resident-weight halo kernel have one tile and are not listed), per batch size, launched alone by "
+         "`fs_bench_conv` "
          f"({WARMUP} untimed + {ITERS} timed launches, Z models per launch, the library's K-split rule; a layer "
          "that carries a projection shortcut is left out: the other layers of its stage have its "
          "shape without the shortcut).  `us`: kernel-trace "
