@@ -570,11 +570,10 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
       has_res ? rsrc(reinterpret_cast<const uint16_t*>(a.res) + z * a.res_mstride, (uint32_t)((int64_t)a.M * a.Cout * 2))
               : rsrc(a.y, 0u);
 
-  // ---- this lane's pixels m = m0 + 32 i + fr: top-left patch position q0,
-  // swizzle key h0 = m, output row mg (-1 past M)
+  // ---- this lane's pixels m = m0 + 32 i + fr: top-left patch position q0
+  // (the swizzle key and the output row are m itself; 0 / none past M)
   const int b0 = fdiv(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv(r0, inv_w);
   const int R0 = b0 * HP + y0;  // padded row above the first pixel
-  // (the swizzle key and the output row are m itself, 0 / none past M)
   int q0[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
@@ -620,11 +619,59 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
     }
   };
 
+  // ---- projection shortcut (a.x2): after the 3x3 reduction, Cin2 / 64 more
+  // K-tiles of the 1x1 conv of x2 at (oy s2, ox s2), each a plain tile of BM
+  // pixel rows x 64 channels loaded into a patch buffer (instruction i of
+  // this wave fills rows (4 i + wave) * 8 .. +8; the lane's 16-byte chunk
+  // lands at chunk (lane & 7) of its row, holding channels ((lane & 7) ^
+  // swz(row)) * 8 .., as in the implicit GEMM)
+  const int NP = a.x2 ? a.Cin2 / BK : 0;
+  const __amdgpu_buffer_rsrc_t rx2 =
+      rsrc(a.x2 ? reinterpret_cast<const uint16_t*>(a.x2) + z * a.x2_mstride : reinterpret_cast<const uint16_t*>(a.x),
+           a.x2 ? (uint32_t)((int64_t)a.B * a.H2 * a.W2 * a.Cin2 * 2) : 0u);
+  uint32_t p2[FM];
+  if (NP > 0) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = (i * HR_NW + wave) * 8 + lr, m = m0 + row;
+      const int lc = (lane & 7) ^ swz(row);
+      if (m < a.M) {
+        const int b = fdiv(m, inv_hw), r = m - b * HW, y = fdiv(r, inv_w), x = r - y * W;
+        p2[i] = (uint32_t)(((((int64_t)b * a.H2 + y * a.stride2) * a.W2 + x * a.stride2) * a.Cin2 + lc * 8) * 2);
+      } else {
+        p2[i] = OOB;
+      }
+    }
+  }
+  auto issue_proj = [&](char* pb, int j) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const uint32_t off = p2[i] == OOB ? OOB : p2[i] + (uint32_t)(j * BK * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx2, (lds_void*)(pb + (i * HR_NW + wave) * 1024), 16, off, 0, 0, 0);
+    }
+  };
+
   floatx16 acc[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+
+  // one projection K-tile: rows 32 i + fr of the tile, weights from wv
+  auto proj_mma = [&](const char* pb, const uint4 (&wv)[4]) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      bf16x8 pf[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int row = i * 32 + fr;
+        pf[i] = *reinterpret_cast<const bf16x8*>(pb + row * ROW + (((2 * kk + fq) ^ swz(row)) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wv[kk]), pf[i], acc[i], 0, 0, 0);
+    }
+  };
 
   // one tap: pixel fragments from the patch (row q0 + ky PW + kx, swizzle
   // key h0 + ky W + kx), weight fragments from wv
@@ -653,22 +700,27 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
   };
 
   // one chunk: nine taps; at tap t the next tap's weights and slice t of
-  // the next chunk's patch are issued, then this tap's MFMAs run, then the
+  // the next chunk's patch are issued (after the last chunk: the first
+  // projection K-tile and its weights), then this tap's MFMAs run, then the
   // wave waits for what it issued; the workgroup meets after the last tap
   uint4 wA[4], wB[4];
   auto chunk = [&](int cc, const char* pcur, char* pnxt, auto par) {
     constexpr int P0 = decltype(par)::value;  // register set of tap 0: 0 = wA, 1 = wB
-    const bool more = cc + 1 < CH;
+    const bool more = cc + 1 < CH, proj = !more && NP > 0;
     static_for<0, 9>([&](auto tc) {
       constexpr int t = decltype(tc)::value;
       constexpr bool inA = ((P0 + t) & 1) == 0;
       if (more) issue_slice(tc, pnxt, cc + 1);
+      if constexpr (t == 0) {
+        if (proj) issue_proj(pnxt, 0);
+      }
       if (t < 8) {
         if constexpr (inA) load_w((t + 1) * CH + cc, wB);
         else load_w((t + 1) * CH + cc, wA);
-      } else if (more) {
-        if constexpr (inA) load_w(cc + 1, wB);
-        else load_w(cc + 1, wA);
+      } else if (more || proj) {
+        const int kt = more ? cc + 1 : 9 * CH;  // the next chunk's tap 0, or the first projection K-tile
+        if constexpr (inA) load_w(kt, wB);
+        else load_w(kt, wA);
       }
       if constexpr (inA) tap_mma(pcur, t, wA);
       else tap_mma(pcur, t, wB);
@@ -685,6 +737,23 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
   for (int cc = 0; cc < CH; cc += 2) {  // chunks in pairs: the patch buffers and register sets by name
     chunk(cc, ps0, ps1, std::integral_constant<int, 0>{});
     chunk(cc + 1, ps1, ps0, std::integral_constant<int, 1>{});
+  }
+  // the projection K-tiles (CH is even: the first is in ps0 and wA), each
+  // with the next one's tile and weights in flight; every wave waits for
+  // its loads, and the workgroup meets before a tile is read and before its
+  // buffer is refilled
+  auto pstep = [&](int j, const char* pcur, char* pnxt, const uint4 (&wc)[4], uint4 (&wn)[4]) {
+    if (j + 1 < NP) {
+      issue_proj(pnxt, j + 1);
+      load_w(9 * CH + j + 1, wn);
+    }
+    proj_mma(pcur, wc);
+    wait_vmcnt<0>();
+    wg_barrier();
+  };
+  for (int j = 0; j < NP; j += 2) {
+    pstep(j, ps0, ps1, wA, wB);
+    if (j + 1 < NP) pstep(j + 1, ps1, ps0, wB, wA);
   }
 
   // ---- epilogue: bias, residual, ReLU, bf16, 16-byte stores (after the
@@ -746,6 +815,19 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
 
 }  // namespace
 
+// A 3x3/1 layer carrying a projection shortcut, in the register-weight
+// form: the 3x3 part as conv_hs_ok requires, then whole 64-channel K-tiles
+// of the shortcut's input at (oy s2, ox s2).
+static bool hr_proj_shape_ok(const ConvArgs& a) {
+  if (!a.x2) return false;
+  ConvArgs m = a;  // the 3x3 part alone
+  m.x2 = nullptr;
+  m.K = m.Kp = a.K1;
+  return conv_hs_ok(m) && a.K1 == 9 * a.Cin && a.Cin2 % BK == 0 && a.K1 + a.Cin2 == a.K && a.K == a.Kp &&
+         (a.Ho - 1) * a.stride2 < a.H2 && (a.Wo - 1) * a.stride2 < a.W2 &&
+         (int64_t)a.B * a.H2 * a.W2 * a.Cin2 * 2 < (1ll << 31) && (int64_t)a.Cout * a.Kp * 2 < (1ll << 31);
+}
+
 bool conv_hs_ok(const ConvArgs& a) {
   if (!(!a.x2 && a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cin % (2 * BK) == 0 && a.K == a.Kp &&
         a.Kp == 9 * a.Cin && a.Ho == a.H && a.Wo == a.W && a.Cout % HS_BN == 0))
@@ -760,12 +842,13 @@ bool conv_hs_ok(const ConvArgs& a) {
 // 64-channel chunk rather than once per tap beats the implicit GEMM there.
 // Shape-only, so a layer's kernel family, and with it the bits of its
 // results, never depends on the device or the batch.
-bool conv_hs_chosen(const ConvArgs& a) { return conv_hs_ok(a); }
+bool conv_hs_chosen(const ConvArgs& a) { return conv_hs_ok(a) || hr_proj_shape_ok(a); }
 
 // The register-weight form needs the fragment-ordered weights and a patch of
-// at most 40 KB (two buffers per workgroup, two workgroups per CU).
+// at most 40 KB (two buffers per workgroup, two workgroups per CU); it also
+// takes a projection shortcut.
 bool conv_hr_ok(const ConvArgs& a, int bm) {
-  if (!conv_hs_ok(a) || !a.wf) return false;
+  if (!(conv_hs_ok(a) || hr_proj_shape_ok(a)) || !a.wf) return false;
   const int64_t need = bm == 160 ? hr_patch_px<160>(a) : bm == 96 ? hr_patch_px<96>(a) : -1;
   return need >= 0 && need <= 8 * HR_NPB[2];
 }
