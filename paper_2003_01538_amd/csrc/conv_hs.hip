@@ -68,11 +68,6 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// floor(n / d) for 0 <= n < 2^22 from a float reciprocal: n + 0.5 is exact,
-// the product carries a relative error below 2^-23, and (n + 0.5) / d lies
-// at least 0.5 / d from an integer, so the truncation is exact.
-__device__ __forceinline__ int fdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
-
 // Patch instructions per wave in slice u of a chunk's nine slices.
 template <int NPBW>
 constexpr int hs_ps(int u) { return NPBW / 9 + (u < NPBW % 9 ? 1 : 0); }
@@ -205,19 +200,19 @@ __global__ void __launch_bounds__(64 * HS_NW, 1) k_conv_hs(ConvArgs a) {
 #pragma unroll
   for (int v = 0; v < NPBW; ++v) {
     const int q = (v * HS_NW + wave) * 8 + lr;
-    q_pr[v] = fdiv(q, inv_pw);
+    q_pr[v] = fdiv_small(q, inv_pw);
     q_pc[v] = q - q_pr[v] * PW;
   }
   // byte offsets (chunk 0) of this lane's patch pixels for tile t; pixels
   // outside the image get an offset past the range for every chunk
   auto patch_offsets = [&](int t, uint32_t (&po)[NPBW]) {
     const int m0 = t * HS_BM;
-    const int b0 = fdiv(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv(r0, inv_w);
+    const int b0 = fdiv_small(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv_small(r0, inv_w);
     const int R0 = b0 * HP + y0;  // padded row above the first pixel
 #pragma unroll
     for (int v = 0; v < NPBW; ++v) {
       const int R = R0 + q_pr[v];
-      const int b = fdiv(R, inv_hp), yy = R - b * HP - 1, xx = q_pc[v] - 1;
+      const int b = fdiv_small(R, inv_hp), yy = R - b * HP - 1, xx = q_pc[v] - 1;
       const int lc = (lane & 7) ^ ((((R - 2 * b) * W + q_pc[v]) >> 1) & 7);
       const bool ok = b < a.B && (unsigned)yy < (unsigned)H && (unsigned)xx < (unsigned)W;
       po[v] = ok ? (uint32_t)(((((int64_t)b * H + yy) * W + xx) * a.Cin + lc * 8) * 2) : OOB;
@@ -238,13 +233,13 @@ __global__ void __launch_bounds__(64 * HS_NW, 1) k_conv_hs(ConvArgs a) {
   // the output row m (-1 past M)
   auto pixel_geom = [&](int t, int (&q0)[2], int (&h0)[2], int (&mg)[2]) {
     const int m0 = t * HS_BM;
-    const int b0 = fdiv(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv(r0, inv_w);
+    const int b0 = fdiv_small(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv_small(r0, inv_w);
     const int R0 = b0 * HP + y0;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int m = m0 + (wm * 2 + i) * 32 + fr;
       if (m < a.M) {
-        const int b = fdiv(m, inv_hw), r = m - b * HW, y = fdiv(r, inv_w), x = r - y * W;
+        const int b = fdiv_small(m, inv_hw), r = m - b * HW, y = fdiv_small(r, inv_w), x = r - y * W;
         const int prow = b * HP + y - R0;  // patch row of the top-left tap
         q0[i] = prow * PW + x;
         h0[i] = m;
@@ -484,15 +479,16 @@ __global__ void __launch_bounds__(64 * HS_NW, 1) k_conv_hs(ConvArgs a) {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
-// Patch pixels the tiles of this layer need: for each tile, through its
-// last pixel's bottom-right tap, plus the two rows above that pixel's row
-// whose band the first pixel's top taps start.
-int64_t hs_patch_px(const ConvArgs& a) {
+// Patch pixels the tiles of BM output pixels of this layer need: for each
+// tile, through its last pixel's bottom-right tap, plus the two rows above
+// that pixel's row whose band the first pixel's top taps start.
+template <int BM>
+int64_t patch_px(const ConvArgs& a) {
   const int64_t HW = (int64_t)a.H * a.W, PW = a.W + 2, HP = a.H + 2;
-  const int64_t tiles = (a.M + HS_BM - 1) / HS_BM;
+  const int64_t tiles = (a.M + BM - 1) / BM;
   int64_t need = 0;
   for (int64_t t = 0; t < tiles; ++t) {
-    const int64_t m0 = t * HS_BM, m1 = std::min<int64_t>(a.M, m0 + HS_BM) - 1;
+    const int64_t m0 = t * BM, m1 = std::min<int64_t>(a.M, m0 + BM) - 1;
     const int64_t R0 = (m0 / HW) * HP + (m0 % HW) / a.W;      // padded row above the first pixel
     const int64_t b1 = m1 / HW, y1 = (m1 % HW) / a.W, x1 = (m1 % HW) % a.W;
     const int64_t q = (b1 * HP + y1 - R0) * PW + x1 + 2 * PW + 2;  // last pixel's bottom-right tap
@@ -500,6 +496,7 @@ int64_t hs_patch_px(const ConvArgs& a) {
   }
   return need;
 }
+int64_t hs_patch_px(const ConvArgs& a) { return patch_px<HS_BM>(a); }
 
 constexpr int HS_NPB[] = {32, 40, 48};  // instantiated patch sizes (8-pixel blocks)
 
@@ -515,26 +512,11 @@ constexpr int HS_NPB[] = {32, 40, 48};  // instantiated patch sizes (8-pixel blo
 // At most 80 KB of LDS and 256 VGPRs, so two workgroups share a CU.  Patch
 // geometry and swizzle as above; per output the sum runs over chunks, then
 // taps, then the 64 channels in MFMA order, as above, so the bits are the
-// same.  Every tap waits for its loads to land (the next tap's weights and a
-// ninth of the next patch, issued one tap earlier).
+// same.  Each tap issues the next tap's weights and a ninth of the next
+// patch, runs its MFMAs and then waits for those loads.
 constexpr int HR_BN = 128;
 constexpr int HR_NW = 4;
 constexpr int HR_NPB[] = {24, 32, 40};  // instantiated patch sizes (8-pixel blocks)
-
-template <int BM>
-int64_t hr_patch_px(const ConvArgs& a) {
-  const int64_t HW = (int64_t)a.H * a.W, PW = a.W + 2, HP = a.H + 2;
-  const int64_t tiles = (a.M + BM - 1) / BM;
-  int64_t need = 0;
-  for (int64_t t = 0; t < tiles; ++t) {
-    const int64_t m0 = t * BM, m1 = std::min<int64_t>(a.M, m0 + BM) - 1;
-    const int64_t R0 = (m0 / HW) * HP + (m0 % HW) / a.W;
-    const int64_t b1 = m1 / HW, y1 = (m1 % HW) / a.W, x1 = (m1 % HW) % a.W;
-    const int64_t q = (b1 * HP + y1 - R0) * PW + x1 + 2 * PW + 2;
-    need = std::max(need, q + 1);
-  }
-  return need;
-}
 
 template <int BM, int NPB>
 __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
@@ -572,14 +554,14 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
 
   // ---- this lane's pixels m = m0 + 32 i + fr: top-left patch position q0
   // (the swizzle key and the output row are m itself; 0 / none past M)
-  const int b0 = fdiv(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv(r0, inv_w);
+  const int b0 = fdiv_small(m0, inv_hw), r0 = m0 - b0 * HW, y0 = fdiv_small(r0, inv_w);
   const int R0 = b0 * HP + y0;  // padded row above the first pixel
   int q0[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int m = m0 + i * 32 + fr;
     if (m < a.M) {
-      const int b = fdiv(m, inv_hw), r = m - b * HW, y = fdiv(r, inv_w), x = r - y * W;
+      const int b = fdiv_small(m, inv_hw), r = m - b * HW, y = fdiv_small(r, inv_w), x = r - y * W;
       q0[i] = (b * HP + y - R0) * PW + x;
     } else {
       q0[i] = 0;
@@ -602,9 +584,9 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
 #pragma unroll
   for (int v = 0; v < NPBW; ++v) {
     const int q = (v * HR_NW + wave) * 8 + lr;
-    const int pr = fdiv(q, inv_pw), pc = q - pr * PW;
+    const int pr = fdiv_small(q, inv_pw), pc = q - pr * PW;
     const int R = R0 + pr;
-    const int b = fdiv(R, inv_hp), yy = R - b * HP - 1, xx = pc - 1;
+    const int b = fdiv_small(R, inv_hp), yy = R - b * HP - 1, xx = pc - 1;
     const int lc = (lane & 7) ^ ((((R - 2 * b) * W + pc) >> 1) & 7);
     const bool ok = b < a.B && (unsigned)yy < (unsigned)H && (unsigned)xx < (unsigned)W;
     po[v] = ok ? (uint32_t)(((((int64_t)b * H + yy) * W + xx) * a.Cin + lc * 8) * 2) : OOB;
@@ -636,7 +618,7 @@ __global__ void __launch_bounds__(64 * HR_NW, 2) k_conv_hr(ConvArgs a) {
       const int row = (i * HR_NW + wave) * 8 + lr, m = m0 + row;
       const int lc = (lane & 7) ^ swz(row);
       if (m < a.M) {
-        const int b = fdiv(m, inv_hw), r = m - b * HW, y = fdiv(r, inv_w), x = r - y * W;
+        const int b = fdiv_small(m, inv_hw), r = m - b * HW, y = fdiv_small(r, inv_w), x = r - y * W;
         p2[i] = (uint32_t)(((((int64_t)b * a.H2 + y * a.stride2) * a.W2 + x * a.stride2) * a.Cin2 + lc * 8) * 2);
       } else {
         p2[i] = OOB;
@@ -849,7 +831,7 @@ bool conv_hs_chosen(const ConvArgs& a) { return conv_hs_ok(a) || hr_proj_shape_o
 // takes a projection shortcut.
 bool conv_hr_ok(const ConvArgs& a, int bm) {
   if (!(conv_hs_ok(a) || hr_proj_shape_ok(a)) || !a.wf) return false;
-  const int64_t need = bm == 160 ? hr_patch_px<160>(a) : bm == 96 ? hr_patch_px<96>(a) : -1;
+  const int64_t need = bm == 160 ? patch_px<160>(a) : bm == 96 ? patch_px<96>(a) : -1;
   return need >= 0 && need <= 8 * HR_NPB[2];
 }
 
@@ -857,7 +839,7 @@ void launch_conv_hr(const ConvArgs& a_in, int bm, hipStream_t s) {
   ConvArgs a = a_in;
   a.split = 1;
   a.partial = nullptr;
-  const int64_t need = bm == 160 ? hr_patch_px<160>(a) : hr_patch_px<96>(a);
+  const int64_t need = bm == 160 ? patch_px<160>(a) : patch_px<96>(a);
   int npb = 0;
   for (int c : HR_NPB)
     if (need <= 8 * c) { npb = c; break; }
