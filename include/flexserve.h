@@ -264,7 +264,9 @@ fs_status fs_profile_launches(fs_ensemble *e, fs_launch_stat *out, int32_t max_o
  * shape key and the tile kept), for every bucket planned so far.  Tiles
  * come from a committed table of such choices per layer shape and batch
  * bucket; only layers the table lacks are timed (environment FS_TUNE=1:
- * time every layer, FS_TUNE=0: never time, the shape rule instead).  Copies at
+ * time every layer, FS_TUNE=3: time every layer with the table's tile kept
+ * unless another wins by 3 %, FS_TUNE=0: never time, the shape rule
+ * instead).  Copies at
  * most n - 1 bytes and a terminating zero into buf (when buf is not NULL and
  * n > 0); *needed (if not NULL) receives the full length + 1.
  * FS_ERR_INVALID for a NULL handle. */

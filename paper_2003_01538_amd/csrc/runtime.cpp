@@ -979,10 +979,17 @@ const std::vector<std::vector<int>>& tiles_for(fs_ensemble* e, int B, hipStream_
       int best = conv_pick_tile(e->prec, a, e->num_cus);
       const int from_table = e->tune == 1 ? -1 : table_tile(e, a, bucket, fam);
       if (from_table >= 0) best = from_table;
-      if (e->tune == 1 || (e->tune == 2 && from_table < 0)) {
+      if (e->tune == 1 || e->tune == 3 || (e->tune == 2 && from_table < 0)) {
+        // re-timing against the table (3): its tile is timed first, so that
+        // another candidate replaces it only by winning by the margin below
+        std::vector<int> order;
+        if (e->tune == 3 && from_table >= 0) order.push_back(from_table);
+        for (int t = 0; t < conv_num_tiles(e->prec); ++t)
+          if (conv_tile_candidate(e->prec, t, a) && conv_tile_family(conv_tile(e->prec, t)) == fam &&
+              !(e->tune == 3 && t == from_table))
+            order.push_back(t);
         float best_ms = 1e30f;
-        for (int t = 0; t < conv_num_tiles(e->prec); ++t) {
-          if (!conv_tile_candidate(e->prec, t, a) || conv_tile_family(conv_tile(e->prec, t)) != fam) continue;
+        for (int t : order) {
           launch_conv(a, e->prec, t, s);
           HIPCHK(hipEventRecord(e0, s));
           launch_conv(a, e->prec, t, s);
